@@ -1,0 +1,6 @@
+"""CPU oracle for the spike-gated INT8 projection (test infrastructure only).
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
+import this package.  The GPU library never uses it.
+"""
+from .spike_oracle import build, load, active_indices, spike_acc, spike_forward  # noqa: F401

@@ -1,0 +1,43 @@
+"""Parser for the hand-worked fixture files in this directory."""
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def load_hand_example(name: str = "hand_worked_example.txt"):
+    Q, scale, masks, acc, out = [], None, [], [], []
+    K = N = None
+    with open(os.path.join(HERE, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            key, *vals = line.split()
+            if key == "K":
+                K = int(vals[0])
+            elif key == "N":
+                N = int(vals[0])
+            elif key == "Q":
+                Q.append([int(v) for v in vals])
+            elif key == "scale_hex":
+                scale = np.array([int(v, 16) for v in vals], dtype=np.uint32).view(np.float32)
+            elif key == "mask_hex":
+                masks.append([int(v, 16) for v in vals])
+            elif key == "acc":
+                acc.append([int(v) for v in vals])
+            elif key == "out_hex":
+                out.append([int(v, 16) for v in vals])
+            else:
+                raise ValueError(f"unknown key {key}")
+    Q = np.array(Q, dtype=np.int8)
+    assert Q.shape == (N, K)
+    return dict(
+        K=K, N=N,
+        W=np.ascontiguousarray(Q.T),  # column-major storage: W[k, n] = Q[n, k]
+        scale=scale,
+        masks=np.array(masks, dtype=np.uint64),
+        acc=np.array(acc, dtype=np.int32),
+        out_bits=np.array(out, dtype=np.uint32),
+    )
