@@ -1,0 +1,155 @@
+/*
+ * spike_proj.h -- C ABI of the MI355X spike-gated INT8 projection library.
+ *
+ * Operation (paper Sec. 2.2 and Sec. 2.3, Eq. (sparse)):
+ *
+ *     y[b][n] = scale[n] * sum_{k : x_b[k] = 1} Q[n][k]
+ *
+ * for binary spike rows x_b in {0,1}^K and INT8 weights Q with N output
+ * channels.  The sum over the active columns is exact in INT32; it is then
+ * converted to FP32 and multiplied once, in binary32 with round-to-nearest-
+ * even and no fused multiply-add, by the per-output-channel FP32 scale.
+ * Results are bit-identical to that definition for every launch
+ * configuration (integer addition is associative, so the order in which
+ * workgroups combine partial sums cannot change them).
+ *
+ * Data layout (all pointers are DEVICE pointers unless stated):
+ *   W      int8   [K][N]  column-major weights: W[k*N + n] = Q[n][k], so the
+ *                         column of input k is N contiguous bytes (Sec. 2.2).
+ *   scale  float  [N]     one FP32 scale per OUTPUT channel (Sec. 2.3).
+ *   mask   uint64 [B][ceil(K/64)]  spike bitmask; bit k of row b is bit
+ *                         (k % 64) of little-endian word (k / 64) of that row
+ *                         (byte-identical to numpy packbits(bitorder=
+ *                         "little") padded to 8-byte rows).  Bits at
+ *                         positions >= K are padding and are ignored.
+ *   out    float  [B][N]  row-major; every element is written.
+ *
+ * Ownership: create() BORROWS W and scale (the caller keeps them alive and
+ * unchanged until destroy()).  The handle owns a small INT32 workspace of
+ * max_B * N entries plus completion counters; the kernels leave it zeroed
+ * after every call, so forward() performs no allocation, memset or host
+ * synchronisation and can be captured into a HIP graph.  A handle must not
+ * run on two streams at the same time (its workspace is shared).
+ *
+ * Errors: every entry point returns SPIKE_OK (0) or a negative code;
+ * spike_proj_last_error() returns a message for the calling thread's last
+ * failure.  Arguments are validated before any HIP call.  No C++ exception
+ * crosses this interface.  Launch failures are reported as SPIKE_EHIP.
+ */
+#ifndef SPIKE_PROJ_H
+#define SPIKE_PROJ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPIKE_OK 0
+#define SPIKE_EINVAL (-1)       /* bad argument (null pointer, size out of range) */
+#define SPIKE_EHIP (-2)         /* a HIP runtime call or kernel launch failed */
+#define SPIKE_ENOMEM (-3)       /* device or host allocation failed */
+#define SPIKE_EUNSUPPORTED (-4) /* valid request this library does not serve */
+
+#define SPIKE_MAX_K (1 << 24) /* keeps every INT32 sum exact: 128 * 2^24 = 2^31 */
+#define SPIKE_MAX_N (1 << 24)
+#define SPIKE_DEFAULT_MAX_B 512
+
+typedef struct spike_proj *spike_proj_t;
+typedef struct spike_stream *spike_stream_t;
+
+/* Create a projection over borrowed column-major INT8 weights W [K][N] and
+ * FP32 scales [N] (Sec. 2.2: binary-input projections are stored
+ * column-major; Sec. 2.3: one scale per output channel).  1 <= K <=
+ * SPIKE_MAX_K, 1 <= N <= SPIKE_MAX_N.  Reserves a workspace for
+ * SPIKE_DEFAULT_MAX_B rows on the current device.  On success *out_handle
+ * is set; on failure it is set to NULL. */
+int spike_proj_create(const int8_t *W_int8_colmajor, const float *scale_fp32, int32_t K, int32_t N,
+                      spike_proj_t *out_handle);
+
+/* Resize the workspace so that forward() accepts up to max_B rows
+ * (1 <= max_B <= 65535).  Allocates; call it outside graph capture and
+ * while no forward() of this handle is in flight. */
+int spike_proj_reserve(spike_proj_t h, int32_t max_B);
+
+/* y = Eq. (sparse) for B spike rows: out[b*N + n].  Asynchronous on
+ * `stream` (a hipStream_t; NULL means the default stream).  B = 0 is a
+ * no-op; 0 <= B <= the reserved max_B.  Dispatches to the active-column
+ * gather (decode-sized B) or to the dense i8 matrix-core contraction over
+ * the 0/1 spike matrix (prefill-sized B); both give identical bits. */
+int spike_proj_forward(spike_proj_t h, const uint64_t *spike_bitmask, int32_t B, float *out_fp32,
+                       void *stream);
+
+/* Same as spike_proj_forward but writes the raw INT32 sums
+ * acc[b*N + n] = sum_{k in A_b} Q[n][k] (the accumulator of Sec. 2.3)
+ * instead of the scaled FP32 outputs.  Used to check the integer path. */
+int spike_proj_forward_acc(spike_proj_t h, const uint64_t *spike_bitmask, int32_t B, int32_t *acc_i32,
+                           void *stream);
+
+/* Release the workspace and the handle (waits for the device first).
+ * NULL is accepted. */
+int spike_proj_destroy(spike_proj_t h);
+
+/* Kernel-path and launch-shape controls, for measurement.  The result never
+ * depends on them.  Keys:
+ *   SPIKE_TUNE_PATH         SPIKE_PATH_AUTO (default), _GATHER or _MFMA
+ *   SPIKE_TUNE_SLICE_WORDS  64-bit mask words per K-slice of the gather
+ *                           (0 = automatic; 1..256)
+ *   SPIKE_TUNE_MFMA_MIN_B   smallest B sent to the matrix-core path by AUTO
+ *   SPIKE_TUNE_VEC          bytes per lane per column load of the gather:
+ *                           0 = automatic, 1, 4, 8 or 16 (16, 8 and 4 need
+ *                           N and the W address to be multiples of it)
+ *   SPIKE_TUNE_MAX_SLICES   cap on K-slices chosen automatically (1..4096)
+ * Returns SPIKE_EINVAL for an unknown key or a value out of range.
+ */
+#define SPIKE_TUNE_PATH 1
+#define SPIKE_TUNE_SLICE_WORDS 2
+#define SPIKE_TUNE_MFMA_MIN_B 3
+#define SPIKE_TUNE_VEC 4
+#define SPIKE_TUNE_MAX_SLICES 5
+#define SPIKE_PATH_AUTO 0
+#define SPIKE_PATH_GATHER 1
+#define SPIKE_PATH_MFMA 2
+int spike_proj_tune(spike_proj_t h, int32_t key, int32_t value);
+
+/* Active-index extraction (Sec. 2.2, A = {k : x_k = 1}) as a standalone
+ * kernel.  For each row b < B writes the ascending active indices to
+ * active_idx[b*K + i], i < active_count[b]; entries past the count are left
+ * untouched.  active_idx is int32 [B][K], active_count is int32 [B]. */
+int spike_compact(const uint64_t *spike_bitmask, int32_t B, int32_t K, int32_t *active_idx,
+                  int32_t *active_count, void *stream);
+
+/* Layer-stack driver (Sec. 2.1: a block runs its TCAM projection and then
+ * its FFN down projection; 22 blocks in order).  Runs projs[0..n_proj) in
+ * order on `stream`, each on B rows.  Spike masks and outputs are packed per
+ * projection, in order: projection j reads B rows of ceil(K_j/64) words
+ * starting at word offset sum_{i<j} B*ceil(K_i/64) of `masks`, and writes
+ * B*N_j floats starting at sum_{i<j} B*N_i of `out`. */
+int spike_stack_forward(const spike_proj_t *projs, int32_t n_proj, const uint64_t *masks, int32_t B,
+                        float *out, void *stream);
+
+/* Throughput mode for many independent batch-1 projections: n_tokens
+ * tokens, each running n_proj projections, all in one launch.  projs holds
+ * n_sets * n_proj handles; token t uses projs[(t % n_sets) * n_proj + j]
+ * (n_sets > 1 rotates address-distinct weight copies).  All handles must
+ * share N.  Per token, masks hold the projections' rows back to back
+ * (token stride sum_j ceil(K_j/64) words) and out holds n_proj * N floats.
+ * create() copies a small descriptor table to the device (allocates);
+ * forward() only launches. */
+int spike_stream_create(const spike_proj_t *projs, int32_t n_proj, int32_t n_sets, int32_t n_tokens,
+                        spike_stream_t *out_stream);
+int spike_stream_forward(spike_stream_t s, const uint64_t *masks, float *out, void *stream);
+int spike_stream_destroy(spike_stream_t s);
+
+/* Message describing the calling thread's most recent failure ("" if none). */
+const char *spike_proj_last_error(void);
+
+/* ABI version of this header. */
+#define SPIKE_PROJ_ABI_VERSION 1
+int spike_proj_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPIKE_PROJ_H */

@@ -1,0 +1,218 @@
+"""ctypes binding of libspike_proj.so (C ABI in include/spike_proj.h).
+
+Argument marshalling only: every step of the projection runs in the HIP
+kernels of the library.  Tensors are torch device tensors; their data
+pointers are passed straight through.  There is no fallback: if the library
+is missing, importing this module fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+from .build import LIB
+
+SPIKE_OK, SPIKE_EINVAL, SPIKE_EHIP, SPIKE_ENOMEM, SPIKE_EUNSUPPORTED = 0, -1, -2, -3, -4
+SPIKE_TUNE_PATH, SPIKE_TUNE_SLICE_WORDS, SPIKE_TUNE_MFMA_MIN_B, SPIKE_TUNE_VEC, SPIKE_TUNE_MAX_SLICES = 1, 2, 3, 4, 5
+SPIKE_PATH_AUTO, SPIKE_PATH_GATHER, SPIKE_PATH_MFMA = 0, 1, 2
+SPIKE_DEFAULT_MAX_B = 512
+
+EXPORTED = (
+    "spike_proj_create", "spike_proj_reserve", "spike_proj_forward", "spike_proj_forward_acc",
+    "spike_proj_destroy", "spike_proj_tune", "spike_compact", "spike_stack_forward",
+    "spike_stream_create", "spike_stream_forward", "spike_stream_destroy", "spike_proj_last_error",
+    "spike_proj_abi_version",
+)
+
+if not os.path.exists(LIB):
+    raise ImportError(f"{LIB} is not built; run __graft_entry__.build() (python -m paper_2606_03026_amd.build)")
+
+_lib = ctypes.CDLL(LIB)
+_p, _i32 = ctypes.c_void_p, ctypes.c_int32
+_sig = {
+    "spike_proj_create": [_p, _p, _i32, _i32, ctypes.POINTER(_p)],
+    "spike_proj_reserve": [_p, _i32],
+    "spike_proj_forward": [_p, _p, _i32, _p, _p],
+    "spike_proj_forward_acc": [_p, _p, _i32, _p, _p],
+    "spike_proj_destroy": [_p],
+    "spike_proj_tune": [_p, _i32, _i32],
+    "spike_compact": [_p, _i32, _i32, _p, _p, _p],
+    "spike_stack_forward": [_p, _i32, _p, _i32, _p, _p],
+    "spike_stream_create": [_p, _i32, _i32, _i32, ctypes.POINTER(_p)],
+    "spike_stream_forward": [_p, _p, _p, _p],
+    "spike_stream_destroy": [_p],
+    "spike_proj_abi_version": [],
+}
+for _name, _args in _sig.items():
+    getattr(_lib, _name).argtypes = _args
+    getattr(_lib, _name).restype = ctypes.c_int
+_lib.spike_proj_last_error.argtypes = []
+_lib.spike_proj_last_error.restype = ctypes.c_char_p
+
+
+class SpikeError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where} failed with code {code}: {spike_proj_last_error()}")
+
+
+def _check(rc: int, where: str) -> None:
+    if rc != SPIKE_OK:
+        raise SpikeError(rc, where)
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dev_ptr(t: torch.Tensor, name: str, nbytes: int | None = None) -> int:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if nbytes is not None and t.numel() * t.element_size() < nbytes:
+        raise ValueError(f"{name} holds {t.numel() * t.element_size()} bytes, needs {nbytes}")
+    return t.data_ptr()
+
+
+def words_per_row(K: int) -> int:
+    return (int(K) + 63) // 64
+
+
+class SpikeProj:
+    """Handle returned by spike_proj_create.  Holds the borrowed W and scale
+    tensors so they outlive the handle."""
+
+    def __init__(self, ptr: int, W: torch.Tensor, scale: torch.Tensor):
+        self.ptr, self.W, self.scale = ptr, W, scale
+        self.K, self.N = W.shape
+        self.max_B = SPIKE_DEFAULT_MAX_B
+
+    def close(self):
+        if self.ptr:
+            _check(_lib.spike_proj_destroy(self.ptr), "spike_proj_destroy")
+            self.ptr = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def spike_proj_create(W: torch.Tensor, scale: torch.Tensor) -> SpikeProj:
+    """W: int8 [K, N] (column-major storage of the [N, K] weight), scale: float32 [N]."""
+    if W.dtype != torch.int8 or W.dim() != 2:
+        raise TypeError("W must be an int8 tensor [K, N]")
+    if scale.dtype != torch.float32 or scale.shape != (W.shape[1],):
+        raise TypeError(f"scale must be float32 [N={W.shape[1]}]")
+    out = _p()
+    _check(_lib.spike_proj_create(_dev_ptr(W, "W"), _dev_ptr(scale, "scale"), W.shape[0], W.shape[1],
+                                  ctypes.byref(out)), "spike_proj_create")
+    return SpikeProj(out.value, W, scale)
+
+
+def spike_proj_reserve(h: SpikeProj, max_B: int) -> None:
+    _check(_lib.spike_proj_reserve(h.ptr, int(max_B)), "spike_proj_reserve")
+    h.max_B = int(max_B)
+
+
+def spike_proj_forward(h: SpikeProj, mask: torch.Tensor, B: int, out: torch.Tensor, stream=None) -> None:
+    """mask: B rows of ceil(K/64) 64-bit words (any integer dtype, same bytes); out: float32 [B, N]."""
+    if out.dtype != torch.float32:
+        raise TypeError("out must be float32")
+    _check(_lib.spike_proj_forward(h.ptr, _dev_ptr(mask, "mask", B * words_per_row(h.K) * 8), int(B),
+                                   _dev_ptr(out, "out", B * h.N * 4), _stream(stream)), "spike_proj_forward")
+
+
+def spike_proj_forward_acc(h: SpikeProj, mask: torch.Tensor, B: int, acc: torch.Tensor, stream=None) -> None:
+    if acc.dtype != torch.int32:
+        raise TypeError("acc must be int32")
+    _check(_lib.spike_proj_forward_acc(h.ptr, _dev_ptr(mask, "mask", B * words_per_row(h.K) * 8), int(B),
+                                       _dev_ptr(acc, "acc", B * h.N * 4), _stream(stream)), "spike_proj_forward_acc")
+
+
+def spike_proj_destroy(h: SpikeProj) -> None:
+    h.close()
+
+
+def spike_proj_tune(h: SpikeProj, key: int, value: int) -> None:
+    _check(_lib.spike_proj_tune(h.ptr, int(key), int(value)), "spike_proj_tune")
+
+
+def spike_compact(mask: torch.Tensor, B: int, K: int, active_idx: torch.Tensor, active_count: torch.Tensor,
+                  stream=None) -> None:
+    if active_idx.dtype != torch.int32 or active_count.dtype != torch.int32:
+        raise TypeError("active_idx and active_count must be int32")
+    _check(_lib.spike_compact(_dev_ptr(mask, "mask", B * words_per_row(K) * 8), int(B), int(K),
+                              _dev_ptr(active_idx, "active_idx", B * K * 4),
+                              _dev_ptr(active_count, "active_count", B * 4), _stream(stream)), "spike_compact")
+
+
+def _handle_array(handles):
+    arr = (_p * len(handles))(*[h.ptr for h in handles])
+    return arr
+
+
+def spike_stack_forward(handles, masks: torch.Tensor, B: int, out: torch.Tensor, stream=None) -> None:
+    """Run the projections in order; masks/out packed per projection (see the header)."""
+    arr = _handle_array(handles)
+    mwords = sum(B * words_per_row(h.K) for h in handles)
+    ofl = sum(B * h.N for h in handles)
+    _check(_lib.spike_stack_forward(arr, len(handles), _dev_ptr(masks, "masks", mwords * 8), int(B),
+                                    _dev_ptr(out, "out", ofl * 4), _stream(stream)), "spike_stack_forward")
+
+
+class SpikeStream:
+    def __init__(self, ptr: int, handles, n_proj: int, n_sets: int, n_tokens: int):
+        self.ptr, self.handles = ptr, list(handles)
+        self.n_proj, self.n_sets, self.n_tokens = n_proj, n_sets, n_tokens
+        self.token_words = sum(words_per_row(h.K) for h in self.handles[:n_proj])
+        self.token_out = sum(h.N for h in self.handles[:n_proj])
+
+    def close(self):
+        if self.ptr:
+            _check(_lib.spike_stream_destroy(self.ptr), "spike_stream_destroy")
+            self.ptr = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def spike_stream_create(handles, n_proj: int, n_sets: int, n_tokens: int) -> SpikeStream:
+    if len(handles) != n_proj * n_sets:
+        raise ValueError("need n_proj * n_sets handles")
+    out = _p()
+    _check(_lib.spike_stream_create(_handle_array(handles), int(n_proj), int(n_sets), int(n_tokens),
+                                    ctypes.byref(out)), "spike_stream_create")
+    return SpikeStream(out.value, handles, n_proj, n_sets, n_tokens)
+
+
+def spike_stream_forward(s: SpikeStream, masks: torch.Tensor, out: torch.Tensor, stream=None) -> None:
+    _check(_lib.spike_stream_forward(s.ptr, _dev_ptr(masks, "masks", s.n_tokens * s.token_words * 8),
+                                     _dev_ptr(out, "out", s.n_tokens * s.token_out * 4), _stream(stream)),
+           "spike_stream_forward")
+
+
+def spike_stream_destroy(s: SpikeStream) -> None:
+    s.close()
+
+
+def spike_proj_last_error() -> str:
+    return _lib.spike_proj_last_error().decode()
+
+
+def spike_proj_abi_version() -> int:
+    return _lib.spike_proj_abi_version()
+
+
+def raw_library():
+    """The loaded ctypes library (for ABI tests that call entry points directly)."""
+    return _lib

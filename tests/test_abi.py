@@ -1,0 +1,79 @@
+"""The C-ABI library: it loads, exports every entry point the header
+declares, and rejects bad arguments before touching the GPU (no GPU needed:
+every call here returns from argument validation)."""
+import ctypes
+import glob
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def sp():
+    from paper_2606_03026_amd import _binding
+    return _binding
+
+
+def declared_functions():
+    names = set()
+    for hdr in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = re.sub(r"/\*.*?\*/", "", open(hdr).read(), flags=re.S)
+        names |= set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(spike_\w+)\s*\(", text, flags=re.M))
+    return sorted(names)
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for required in ("spike_proj_create", "spike_proj_forward", "spike_proj_destroy"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(sp):
+    lib = sp.raw_library()
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, f"not exported: {missing}"
+    assert set(sp.EXPORTED) == set(declared_functions())
+
+
+def test_abi_version(sp):
+    assert sp.spike_proj_abi_version() == 1
+
+
+def test_argument_validation_before_any_hip_call(sp):
+    lib = sp.raw_library()
+    out = ctypes.c_void_p()
+    dummy = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    assert lib.spike_proj_create(None, dummy, 4, 4, ctypes.byref(out)) == sp.SPIKE_EINVAL
+    assert out.value is None
+    assert "null" in sp.spike_proj_last_error()
+    assert lib.spike_proj_create(dummy, dummy, 0, 4, ctypes.byref(out)) == sp.SPIKE_EINVAL
+    assert lib.spike_proj_create(dummy, dummy, 4, 0, ctypes.byref(out)) == sp.SPIKE_EINVAL
+    assert lib.spike_proj_create(dummy, dummy, (1 << 24) + 1, 4, ctypes.byref(out)) == sp.SPIKE_EINVAL
+    assert "K" in sp.spike_proj_last_error()
+    assert lib.spike_proj_create(dummy, dummy, 4, 4, None) == sp.SPIKE_EINVAL
+    assert lib.spike_proj_forward(None, dummy, 1, dummy, None) == sp.SPIKE_EINVAL
+    assert lib.spike_proj_forward_acc(None, dummy, 1, dummy, None) == sp.SPIKE_EINVAL
+    assert lib.spike_proj_reserve(None, 8) == sp.SPIKE_EINVAL
+    assert lib.spike_proj_tune(None, sp.SPIKE_TUNE_PATH, 0) == sp.SPIKE_EINVAL
+    assert lib.spike_proj_destroy(None) == sp.SPIKE_OK
+    assert lib.spike_compact(dummy, -1, 64, dummy, dummy, None) == sp.SPIKE_EINVAL
+    assert lib.spike_compact(dummy, 1, 0, dummy, dummy, None) == sp.SPIKE_EINVAL
+    assert lib.spike_compact(dummy, 0, 64, None, None, None) == sp.SPIKE_OK  # B = 0 is a no-op
+    assert lib.spike_stack_forward(None, 2, dummy, 1, dummy, None) == sp.SPIKE_EINVAL
+    assert lib.spike_stream_create(None, 2, 1, 1, ctypes.byref(out)) == sp.SPIKE_EINVAL
+    assert lib.spike_stream_forward(None, dummy, dummy, None) == sp.SPIKE_EINVAL
+    assert lib.spike_stream_destroy(None) == sp.SPIKE_OK
+
+
+def test_product_path_never_touches_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2606_03026_amd")
+    for path in glob.glob(os.path.join(pkg, "**", "*"), recursive=True):
+        if os.path.isfile(path) and path.endswith((".py", ".hip", ".hpp", ".h", ".cpp")):
+            text = open(path).read()
+            assert not re.search(r"^\s*(import|from)\s+oracle", text, flags=re.M), path
+            assert "spike_oracle" not in text, path
+    hdr = open(os.path.join(ROOT, "include", "spike_proj.h")).read()
+    assert "oracle" not in hdr

@@ -1,0 +1,427 @@
+"""GPU parity: the HIP library, called through its C ABI, against the CPU
+oracle on the same seeded inputs.  The bar is bit-exactness of both the
+INT32 accumulators and the FP32 outputs (one scale multiply per output).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_03026_amd import workloads as wl
+from tests.golden.load import load_hand_example
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def sp():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2606_03026_amd import _binding
+    return _binding
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def dmask(m):
+    return dev(np.ascontiguousarray(m, dtype=np.uint64).view(np.int64))
+
+
+def bits32(a):
+    return np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+
+
+def gpu_forward(sp, h, masks, B=None):
+    B = masks.shape[0] if B is None else B
+    out = torch.full((max(B, 1), h.N), float("nan"), dtype=torch.float32, device="cuda")
+    sp.spike_proj_forward(h, dmask(masks), B, out)
+    torch.cuda.synchronize()
+    return out[:B].cpu().numpy()
+
+
+def gpu_acc(sp, h, masks):
+    B = masks.shape[0]
+    acc = torch.full((B, h.N), -7, dtype=torch.int32, device="cuda")
+    sp.spike_proj_forward_acc(h, dmask(masks), B, acc)
+    torch.cuda.synchronize()
+    return acc.cpu().numpy()
+
+
+def assert_parity(sp, h, W, scale, masks, threads=8):
+    ref_acc = oracle.spike_acc(W, masks)
+    ref_out = oracle.spike_forward(W, scale, masks, threads=threads)
+    got_acc = gpu_acc(sp, h, masks)
+    got_out = gpu_forward(sp, h, masks)
+    np.testing.assert_array_equal(got_acc, ref_acc)
+    mism = bits32(got_out) != bits32(ref_out)
+    assert not mism.any(), f"{int(mism.sum())} FP32 outputs differ, first at {np.argwhere(mism)[0]}"
+
+
+def make(sp, W, scale):
+    Wd, sd = dev(W), dev(scale)
+    return sp.spike_proj_create(Wd, sd), Wd, sd
+
+
+# Launch shapes exercised for every small case: (vector bytes per lane, mask
+# words per K-slice); 0 means the automatic choice.
+SHAPES = [(0, 0), (1, 1), (0, 1), (4, 3)]
+
+
+def apply_shape(sp, h, vec, sw):
+    if vec:
+        try:
+            sp.spike_proj_tune(h, sp.SPIKE_TUNE_VEC, vec)
+        except sp.SpikeError:
+            return False
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_SLICE_WORDS, sw)
+    return True
+
+
+def test_hand_worked_example(sp):
+    g = load_hand_example()
+    h, *_ = make(sp, g["W"], g["scale"])
+    for vec, sw in SHAPES:
+        if not apply_shape(sp, h, vec, sw):
+            continue
+        np.testing.assert_array_equal(gpu_acc(sp, h, g["masks"]), g["acc"])
+        np.testing.assert_array_equal(bits32(gpu_forward(sp, h, g["masks"])), g["out_bits"])
+
+
+@pytest.mark.parametrize("K", [1, 63, 64, 65, 200, 1000, 4097])
+@pytest.mark.parametrize("N", [1, 7, 64, 100, 512, 1000, 1536])
+def test_small_shapes(sp, K, N):
+    p = wl.small_problem(K, N, 5, 0.3, seed=K + 7 * N)
+    h, *_ = make(sp, p["W"], p["scale"])
+    for vec, sw in SHAPES:
+        if apply_shape(sp, h, vec, sw):
+            assert_parity(sp, h, p["W"], p["scale"], p["masks"])
+
+
+@pytest.mark.parametrize("vec", [16, 8, 4, 1])
+def test_every_vector_width_on_the_decode_shape(sp, vec):
+    d = wl.single_projection(n_masks=6)
+    h, *_ = make(sp, d["W"], d["scale"])
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_VEC, vec)
+    for sw in (0, 1, 5, 24):
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_SLICE_WORDS, sw)
+        assert_parity(sp, h, d["W"], d["scale"], d["masks"])
+
+
+def test_single_projection_batch1(sp):
+    """1536 -> 1536, Bernoulli(0.10): independent batch-1 calls, then one batch."""
+    d = wl.single_projection(n_masks=32)
+    h, *_ = make(sp, d["W"], d["scale"])
+    ref = oracle.spike_forward(d["W"], d["scale"], d["masks"])
+    for i in range(32):
+        got = gpu_forward(sp, h, d["masks"][i:i + 1])
+        np.testing.assert_array_equal(bits32(got), bits32(ref[i:i + 1]))
+    assert_parity(sp, h, d["W"], d["scale"], d["masks"])
+
+
+@pytest.mark.parametrize("p", wl.DOWN_SWEEP_RATES)
+def test_down_projection_sweep(sp, p):
+    d = wl.down_sweep(p, n_masks=8)
+    h, *_ = make(sp, d["W"], d["scale"])
+    ref = oracle.spike_forward(d["W"], d["scale"], d["masks"])
+    for i in range(8):
+        np.testing.assert_array_equal(bits32(gpu_forward(sp, h, d["masks"][i:i + 1])), bits32(ref[i:i + 1]))
+    assert_parity(sp, h, d["W"], d["scale"], d["masks"])
+
+
+@pytest.fixture(scope="module")
+def stack(sp):
+    """All 44 projections of the 22-block decode stack on the device."""
+    hs, host = [], []
+    for (l, j) in wl.stack_order():
+        W, s = wl.stack_projection(l, j)
+        h, Wd, sd = make(sp, W, s)
+        hs.append(h)
+        host.append((W, s))
+    return hs, host
+
+
+def test_stack_driver_in_order(sp, stack):
+    hs, host = stack
+    T = 3
+    masks = wl.stack_token_masks(T)
+    per_tok_out = sum(h.N for h in hs)
+    for t in range(T):
+        out = torch.full((per_tok_out,), float("nan"), device="cuda")
+        sp.spike_stack_forward(hs, dmask(masks[t]), 1, out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        moff = ooff = 0
+        for h, (W, s) in zip(hs, host):
+            wpr = wl.words_per_row(h.K)
+            ref = oracle.spike_forward(W, s, masks[t:t + 1, moff:moff + wpr])[0]
+            np.testing.assert_array_equal(bits32(got[ooff:ooff + h.N]), bits32(ref))
+            moff += wpr
+            ooff += h.N
+
+
+@pytest.mark.parametrize("n_sets", [1, 2])
+def test_stream_small(sp, stack, n_sets):
+    hs, host = stack
+    if n_sets == 2:  # a second, address-distinct copy of every weight
+        copies = [make(sp, W, s)[0] for (W, s) in host]
+        hs_all, host_all = hs + copies, host + host
+    else:
+        hs_all, host_all = hs, host
+    T = 5
+    masks = wl.stack_token_masks(T)
+    st = sp.spike_stream_create(hs_all, 44, n_sets, T)
+    out = torch.full((T, 44 * 1536), float("nan"), device="cuda")
+    sp.spike_stream_forward(st, dmask(masks), out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    for t in range(T):
+        moff = 0
+        for j, (W, s) in enumerate(host_all[:44]):
+            wpr = wl.words_per_row(W.shape[0])
+            ref = oracle.spike_forward(W, s, masks[t:t + 1, moff:moff + wpr])[0]
+            np.testing.assert_array_equal(bits32(got[t, j * 1536:(j + 1) * 1536]), bits32(ref))
+            moff += wpr
+
+
+def test_stream_full_workload_sampled(sp, stack):
+    """The benchmark's configuration: 1000 tokens x 44 projections in one
+    launch over rotated weight copies; sampled (token, projection) outputs
+    are checked one by one against the oracle."""
+    import bench
+    hs, host = stack
+    n_sets = bench.DEFAULT_SETS
+    extra = []
+    for _ in range(n_sets - 1):
+        for h in hs:  # address-distinct device copies of the same weights
+            c = sp.spike_proj_create(h.W.clone(), h.scale.clone())
+            sp.spike_proj_reserve(c, 1)
+            extra.append(c)
+    T = 1000
+    masks = wl.stack_token_masks(T)
+    st = sp.spike_stream_create(hs + extra, 44, n_sets, T)
+    out = torch.full((T, 44 * 1536), float("nan"), device="cuda")
+    sp.spike_stream_forward(st, dmask(masks), out)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(123)
+    picks = [(0, j) for j in range(44)] + [(T - 1, j) for j in range(44)]
+    picks += [(int(t), int(j)) for t, j in zip(rng.integers(0, T, 60), rng.integers(0, 44, 60))]
+    offs = np.cumsum([0] + [wl.words_per_row(W.shape[0]) for (W, _) in host])
+    for t, j in picks:
+        W, s = host[j]
+        ref = oracle.spike_forward(W, s, masks[t:t + 1, offs[j]:offs[j + 1]])[0]
+        got = out[t, j * 1536:(j + 1) * 1536].cpu().numpy()
+        np.testing.assert_array_equal(bits32(got), bits32(ref), err_msg=f"token {t} projection {j}")
+    assert not torch.isnan(out).any()
+
+
+def test_prefill_batch(sp):
+    """512 tokens x 6144 -> 1536, Markov spikes at rate 0.10."""
+    d = wl.prefill_projection()
+    h, *_ = make(sp, d["W"], d["scale"])
+    for path in (sp.SPIKE_PATH_GATHER, sp.SPIKE_PATH_AUTO):
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, path)
+        assert_parity(sp, h, d["W"], d["scale"], d["masks"])
+
+
+def test_batched_decode_stack(sp):
+    """B = 64 rows through all 44 projections, structured spikes, two steps."""
+    hs, host, masks_by_step = [], [], []
+    for (l, j) in wl.stack_order():
+        W, s = wl.batched_stack_projection(l, j)
+        hs.append(make(sp, W, s)[0])
+        host.append((W, s))
+    bits = [wl.batched_stack_bits(l, j, B=64, n_steps=2) for (l, j) in wl.stack_order()]
+    for step in range(2):
+        masks = np.concatenate([wl.pack_bits(b[step]).reshape(-1) for b in bits])
+        out = torch.full((sum(64 * h.N for h in hs),), float("nan"), device="cuda")
+        sp.spike_stack_forward(hs, dmask(masks), 64, out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        ooff = 0
+        for (W, s), b in zip(host, bits):
+            ref = oracle.spike_forward(W, s, wl.pack_bits(b[step]), threads=8)
+            np.testing.assert_array_equal(bits32(got[ooff:ooff + ref.size]), bits32(ref.reshape(-1)))
+            ooff += ref.size
+
+
+def test_batch_zero_is_a_noop(sp):
+    p = wl.small_problem(100, 64, 1, 0.5)
+    h, *_ = make(sp, p["W"], p["scale"])
+    out = torch.full((1, 64), 3.0, device="cuda")
+    sp.spike_proj_forward(h, dmask(p["masks"]), 0, out)
+    torch.cuda.synchronize()
+    assert (out == 3.0).all()
+
+
+@pytest.mark.parametrize("K,N", [(1536, 1536), (6144, 1536), (77, 33)])
+def test_degenerate_spike_patterns(sp, K, N):
+    rng = np.random.default_rng(K)
+    W = rng.integers(-128, 127, size=(K, N), dtype=np.int8, endpoint=True)
+    scale = wl.uniform_scales(rng, N)
+    bits = np.zeros((4, K), bool)
+    bits[1] = True                      # all active
+    bits[2, K - 1] = True               # only the last column
+    bits[3, 0] = True                   # only the first column
+    masks = wl.pack_bits(bits)
+    if K % 64:                          # junk in the padding bits of every row
+        masks[:, -1] |= np.uint64((~((1 << (K % 64)) - 1)) & 0xFFFFFFFFFFFFFFFF)
+    h, *_ = make(sp, W, scale)
+    for vec, sw in SHAPES:
+        if apply_shape(sp, h, vec, sw):
+            assert_parity(sp, h, W, scale, masks)
+    out = gpu_forward(sp, h, masks[:1])
+    assert not bits32(out).any()        # +0.0 for an empty spike set
+
+
+def test_extreme_values(sp):
+    """-128 weights, subnormal and tiny scales (no flush to zero)."""
+    K, N = 1024, 256
+    W = np.full((K, N), -128, np.int8)
+    W[:, 1::2] = 127
+    scale = np.full(N, 2.0 ** -140, np.float32)
+    scale[::3] = 2.0 ** -149
+    scale[1::5] = 1e-2
+    masks = wl.pack_bits(np.ones((2, K), bool))
+    h, *_ = make(sp, W, scale)
+    assert_parity(sp, h, W, scale, masks)
+    out = gpu_forward(sp, h, masks[:1])
+    assert bits32(out).any()
+
+
+@pytest.mark.parametrize("case", ["int32_min", "above_2_24"])
+def test_maximum_K(sp, case):
+    """K = 2^24 (the largest accepted): the INT32 sum reaches -2^31 exactly,
+    and a sum of 2^24 + 1 must round to nearest even in the conversion."""
+    K, N = 1 << 24, 1
+    if case == "int32_min":
+        W = np.full((K, N), -128, np.int8)
+    else:
+        W = np.ones((K, N), np.int8)
+        W[0, 0] = 2
+    scale = np.array([0.5], np.float32)
+    masks = wl.pack_bits(np.ones((1, K), bool))
+    h, *_ = make(sp, W, scale)
+    ref = oracle.spike_acc(W, masks)
+    assert ref[0, 0] == (-(1 << 31) if case == "int32_min" else (1 << 24) + 1)
+    assert_parity(sp, h, W, scale, masks)
+
+
+def test_repeat_runs_are_bit_identical(sp):
+    d = wl.down_sweep(0.2, n_masks=4)
+    h, *_ = make(sp, d["W"], d["scale"])
+    ref = None
+    for sw in (0, 1, 2, 7, 96):
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_SLICE_WORDS, sw)
+        for _ in range(4):
+            out = bits32(gpu_forward(sp, h, d["masks"]))
+            if ref is None:
+                ref = out
+            np.testing.assert_array_equal(out, ref)
+
+
+def test_workspace_resets_between_calls(sp):
+    """Back-to-back split-K calls on one handle with changing B: a workspace
+    or counter left dirty by one call would corrupt the next."""
+    d = wl.down_sweep(0.1, n_masks=40)
+    h, *_ = make(sp, d["W"], d["scale"])
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_SLICE_WORDS, 1)
+    ref = oracle.spike_forward(d["W"], d["scale"], d["masks"])
+    outs, lo = [], 0
+    stream_out = []
+    for B in (1, 7, 3, 16, 1, 12):
+        out = torch.empty((B, 1536), device="cuda")
+        sp.spike_proj_forward(h, dmask(d["masks"][lo:lo + B]), B, out)   # no sync between calls
+        stream_out.append((lo, B, out))
+        lo += B
+    torch.cuda.synchronize()
+    for lo, B, out in stream_out:
+        np.testing.assert_array_equal(bits32(out.cpu().numpy()), bits32(ref[lo:lo + B]))
+
+
+def test_row_major_weights_fail_parity(sp):
+    """Passing the row-major [N, K] bytes where the column-major [K, N] layout
+    is expected (K != N) must show up as a parity failure."""
+    K, N = 96, 64
+    p = wl.small_problem(K, N, 4, 0.4, seed=1)
+    wrong = np.ascontiguousarray(p["W"].T).reshape(K, N)  # same bytes count, row-major order
+    h, *_ = make(sp, wrong, p["scale"])
+    got = gpu_forward(sp, h, p["masks"])
+    ref = oracle.spike_forward(p["W"], p["scale"], p["masks"])
+    assert (bits32(got) != bits32(ref)).any()
+
+
+def test_side_stream_and_graph_replay(sp):
+    hs, host = [], []
+    for K in (1536, 6144, 1536):
+        p = wl.small_problem(K, 1536, 1, 0.1, seed=K)
+        hs.append(make(sp, p["W"], p["scale"])[0])
+        host.append((p["W"], p["scale"]))
+    words = sum(wl.words_per_row(h.K) for h in hs)
+    static_mask = torch.zeros(words, dtype=torch.int64, device="cuda")
+    static_out = torch.zeros(3 * 1536, device="cuda")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm up on a non-default stream
+        sp.spike_stack_forward(hs, static_mask, 1, static_out)
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        sp.spike_stack_forward(hs, static_mask, 1, static_out)
+    rng = np.random.default_rng(3)
+    for replay in range(4):
+        bits = [rng.random((1, h.K)) < 0.15 for h in hs]
+        m = np.concatenate([wl.pack_bits(b).reshape(-1) for b in bits])
+        static_mask.copy_(dmask(m))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = static_out.cpu().numpy()
+        for j, ((W, s), b) in enumerate(zip(host, bits)):
+            ref = oracle.spike_forward(W, s, wl.pack_bits(b))[0]
+            np.testing.assert_array_equal(bits32(got[j * 1536:(j + 1) * 1536]), bits32(ref), err_msg=f"replay {replay}")
+        # eager work between replays on the same handles
+        eager = torch.zeros(3 * 1536, device="cuda")
+        sp.spike_stack_forward(hs, static_mask, 1, eager)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(bits32(eager.cpu().numpy()), bits32(got))
+
+
+@pytest.mark.parametrize("K", [1, 64, 65, 1536, 6144, 20000])
+def test_compaction_kernel(sp, K):
+    rng = np.random.default_rng(K)
+    bits = rng.random((6, K)) < np.array([0.0, 1.0, 0.02, 0.1, 0.4, 0.9])[:, None]
+    masks = wl.pack_bits(bits)
+    if K % 64:
+        masks[:, -1] |= np.uint64((~((1 << (K % 64)) - 1)) & 0xFFFFFFFFFFFFFFFF)
+    idx = torch.full((6, K), -1, dtype=torch.int32, device="cuda")
+    cnt = torch.full((6,), -1, dtype=torch.int32, device="cuda")
+    sp.spike_compact(dmask(masks), 6, K, idx, cnt)
+    torch.cuda.synchronize()
+    idx, cnt = idx.cpu().numpy(), cnt.cpu().numpy()
+    for b in range(6):
+        ref = oracle.active_indices(masks[b], K)
+        assert cnt[b] == len(ref)
+        np.testing.assert_array_equal(idx[b, :cnt[b]], ref)
+
+
+def test_errors_on_gpu(sp):
+    p = wl.small_problem(128, 64, 1, 0.5)
+    h, *_ = make(sp, p["W"], p["scale"])
+    out = torch.empty((600, 64), device="cuda")
+    masks = torch.zeros((600, 2), dtype=torch.int64, device="cuda")
+    with pytest.raises(sp.SpikeError) as e:
+        sp.spike_proj_forward(h, masks, 513, out)
+    assert e.value.code == sp.SPIKE_EINVAL
+    sp.spike_proj_reserve(h, 600)
+    sp.spike_proj_forward(h, masks, 600, out)
+    torch.cuda.synchronize()
+    assert not bits32(out.cpu().numpy()).any()
+    for key, val in ((sp.SPIKE_TUNE_PATH, 9), (sp.SPIKE_TUNE_SLICE_WORDS, 257), (sp.SPIKE_TUNE_VEC, 3), (99, 0)):
+        with pytest.raises(sp.SpikeError):
+            sp.spike_proj_tune(h, key, val)
+    q = wl.small_problem(128, 32, 1, 0.5)
+    h2, *_ = make(sp, q["W"], q["scale"])
+    with pytest.raises(sp.SpikeError) as e:
+        sp.spike_stream_create([h, h2], 2, 1, 4)
+    assert e.value.code == sp.SPIKE_EUNSUPPORTED
