@@ -100,6 +100,15 @@ int spike_proj_destroy(spike_proj_t h);
  *                           0 = automatic, 1, 4, 8 or 16 (16, 8 and 4 need
  *                           N and the W address to be multiples of it)
  *   SPIKE_TUNE_MAX_SLICES   cap on K-slices chosen automatically (1..4096)
+ *   SPIKE_TUNE_SHAPE        full gather launch shape, SPIKE_SHAPE(V, LG, U,
+ *                           BLOCK): V bytes per lane per column, LG lanes per
+ *                           column group, U columns in flight per group,
+ *                           BLOCK threads per workgroup; 0 = automatic.  Only
+ *                           the shapes the library instantiates are accepted.
+ *   SPIKE_TUNE_TILES_PER_UNIT  output-channel tiles handled by one workgroup
+ *                           (1..4096); the active list is built once per unit
+ *   SPIKE_TUNE_XCD_SPREAD   streams only: 1 = plain unit order; 8 = keep the
+ *                           tiles of one (token, projection) on one XCD
  * Returns SPIKE_EINVAL for an unknown key or a value out of range.
  */
 #define SPIKE_TUNE_PATH 1
@@ -107,10 +116,20 @@ int spike_proj_destroy(spike_proj_t h);
 #define SPIKE_TUNE_MFMA_MIN_B 3
 #define SPIKE_TUNE_VEC 4
 #define SPIKE_TUNE_MAX_SLICES 5
+#define SPIKE_TUNE_SHAPE 6
+#define SPIKE_TUNE_TILES_PER_UNIT 7
+#define SPIKE_TUNE_XCD_SPREAD 8
+#define SPIKE_SHAPE(V, LG, U, BLOCK) ((V) | ((LG) << 5) | ((U) << 15) | (((BLOCK) / 64) << 20))
+#define SPIKE_SHAPE_NT (1 << 25) /* or-ed into a shape code: nontemporal weight loads */
 #define SPIKE_PATH_AUTO 0
 #define SPIKE_PATH_GATHER 1
 #define SPIKE_PATH_MFMA 2
 int spike_proj_tune(spike_proj_t h, int32_t key, int32_t value);
+
+/* The launch-shape codes this build instantiates: writes up to `cap` codes
+ * to `codes` (host memory; may be NULL when cap is 0) and returns how many
+ * exist. */
+int spike_proj_shapes(int32_t *codes, int32_t cap);
 
 /* Active-index extraction (Sec. 2.2, A = {k : x_k = 1}) as a standalone
  * kernel.  For each row b < B writes the ascending active indices to
@@ -139,6 +158,9 @@ int spike_stack_forward(const spike_proj_t *projs, int32_t n_proj, const uint64_
 int spike_stream_create(const spike_proj_t *projs, int32_t n_proj, int32_t n_sets, int32_t n_tokens,
                         spike_stream_t *out_stream);
 int spike_stream_forward(spike_stream_t s, const uint64_t *masks, float *out, void *stream);
+/* Launch-shape controls of a stream (SPIKE_TUNE_SHAPE, SPIKE_TUNE_TILES_PER_UNIT
+ * as for spike_proj_tune); results never depend on them. */
+int spike_stream_tune(spike_stream_t s, int32_t key, int32_t value);
 int spike_stream_destroy(spike_stream_t s);
 
 /* Message describing the calling thread's most recent failure ("" if none). */

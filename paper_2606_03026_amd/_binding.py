@@ -16,13 +16,21 @@ from .build import LIB
 
 SPIKE_OK, SPIKE_EINVAL, SPIKE_EHIP, SPIKE_ENOMEM, SPIKE_EUNSUPPORTED = 0, -1, -2, -3, -4
 SPIKE_TUNE_PATH, SPIKE_TUNE_SLICE_WORDS, SPIKE_TUNE_MFMA_MIN_B, SPIKE_TUNE_VEC, SPIKE_TUNE_MAX_SLICES = 1, 2, 3, 4, 5
+SPIKE_TUNE_SHAPE, SPIKE_TUNE_TILES_PER_UNIT, SPIKE_TUNE_XCD_SPREAD = 6, 7, 8
+SPIKE_SHAPE_NT = 1 << 25
 SPIKE_PATH_AUTO, SPIKE_PATH_GATHER, SPIKE_PATH_MFMA = 0, 1, 2
 SPIKE_DEFAULT_MAX_B = 512
+
+
+def SPIKE_SHAPE(V: int, LG: int, U: int, BLOCK: int, NT: bool = False) -> int:
+    """Shape code of the gather launch (same packing as the header macro)."""
+    return V | (LG << 5) | (U << 15) | ((BLOCK // 64) << 20) | (SPIKE_SHAPE_NT if NT else 0)
 
 EXPORTED = (
     "spike_proj_create", "spike_proj_reserve", "spike_proj_forward", "spike_proj_forward_acc",
     "spike_proj_destroy", "spike_proj_tune", "spike_compact", "spike_stack_forward",
-    "spike_stream_create", "spike_stream_forward", "spike_stream_destroy", "spike_proj_last_error",
+    "spike_stream_create", "spike_stream_forward", "spike_stream_tune", "spike_stream_destroy",
+    "spike_proj_last_error", "spike_proj_shapes",
     "spike_proj_abi_version",
 )
 
@@ -42,8 +50,10 @@ _sig = {
     "spike_stack_forward": [_p, _i32, _p, _i32, _p, _p],
     "spike_stream_create": [_p, _i32, _i32, _i32, ctypes.POINTER(_p)],
     "spike_stream_forward": [_p, _p, _p, _p],
+    "spike_stream_tune": [_p, _i32, _i32],
     "spike_stream_destroy": [_p],
     "spike_proj_abi_version": [],
+    "spike_proj_shapes": [_p, _i32],
 }
 for _name, _args in _sig.items():
     getattr(_lib, _name).argtypes = _args
@@ -201,12 +211,24 @@ def spike_stream_forward(s: SpikeStream, masks: torch.Tensor, out: torch.Tensor,
            "spike_stream_forward")
 
 
+def spike_stream_tune(s: SpikeStream, key: int, value: int) -> None:
+    _check(_lib.spike_stream_tune(s.ptr, int(key), int(value)), "spike_stream_tune")
+
+
 def spike_stream_destroy(s: SpikeStream) -> None:
     s.close()
 
 
 def spike_proj_last_error() -> str:
     return _lib.spike_proj_last_error().decode()
+
+
+def spike_proj_shapes() -> list:
+    """Launch-shape codes instantiated by the library."""
+    n = _lib.spike_proj_shapes(None, 0)
+    buf = (ctypes.c_int32 * n)()
+    _lib.spike_proj_shapes(buf, n)
+    return list(buf)
 
 
 def spike_proj_abi_version() -> int:

@@ -18,6 +18,9 @@
 #include "gather.hpp"
 #include "mfma.hpp"
 
+struct spike_proj;
+struct spike_stream;
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -33,45 +36,110 @@ int fail(int code, const char* fmt, ...)
     return code;
 }
 
-int hip_fail(hipError_t e, const char* what)
-{
-    return fail(SPIKE_EHIP, "%s: %s", what, hipGetErrorString(e));
-}
+int hip_fail(hipError_t e, const char* what) { return fail(SPIKE_EHIP, "%s: %s", what, hipGetErrorString(e)); }
 
 int64_t words_per_row(int64_t K) { return (K + 63) / 64; }
 
-// Launch shapes of the gather: V bytes per lane, LG lanes per column group.
-enum GatherShape { SHAPE_V16_LG32 = 16, SHAPE_V8_LG64 = 8, SHAPE_V4_LG64 = 4, SHAPE_V1_LG64 = 1 };
+// ---------------------------------------------------------------------------
+// Launch shapes.  Every instantiated (V, LG, U, BLOCK) combination of the
+// gather and stream kernels is listed once; a shape code packs it as
+// SPIKE_SHAPE(V, LG, U, BLOCK) from the header.
+// ---------------------------------------------------------------------------
+using GatherFn = void (*)(const spike_proj*, const uint64_t*, int32_t, int, int, int, int, float*, int32_t*,
+                          hipStream_t);
+using StreamFn = void (*)(const spike_stream*, int, unsigned, const uint64_t*, float*, hipStream_t);
 
-int shape_tile(int shape)
+struct ShapeEntry {
+    int code;
+    int vec, lanes, unroll, block;
+    GatherFn gather;
+    GatherFn gather_acc;
+    StreamFn stream;
+};
+
+template <class S, bool ACC>
+void launch_gather_t(const spike_proj* h, const uint64_t* mask, int32_t B, int sw, int n_slices, int n_tiles,
+                     int tpu, float* out, int32_t* acc, hipStream_t st);
+template <class S>
+void launch_stream_t(const spike_stream* s, int n_tiles, unsigned units, const uint64_t* masks, float* out,
+                     hipStream_t st);
+
+template <int V, int LG, int U, int BLOCK, bool NT = false>
+constexpr ShapeEntry entry()
 {
-    switch (shape) {
-    case SHAPE_V16_LG32: return 16 * 32;
-    case SHAPE_V8_LG64: return 8 * 64;
-    case SHAPE_V4_LG64: return 4 * 64;
-    default: return 64;
-    }
+    using S = spk::Shape<V, LG, U, BLOCK, NT>;
+    return ShapeEntry{SPIKE_SHAPE(V, LG, U, BLOCK) | (NT ? SPIKE_SHAPE_NT : 0), V, LG, U, BLOCK,
+                      &launch_gather_t<S, false>, &launch_gather_t<S, true>, &launch_stream_t<S>};
 }
 
-// Widest vector whose loads stay aligned and in range for this matrix.
-int pick_shape(const void* W, int64_t N, int requested)
+const ShapeEntry kShapes[] = {
+    // half-column tiles, nontemporal weight loads (throughput: streams, batched rows)
+    entry<16, 32, 2, 256, true>(), entry<16, 32, 1, 256, true>(), entry<16, 32, 3, 256, true>(),
+    entry<16, 32, 4, 256, true>(), entry<16, 32, 2, 512, true>(), entry<16, 32, 2, 128, true>(),
+    entry<16, 64, 2, 256, true>(), entry<16, 16, 2, 256, true>(), entry<8, 64, 4, 256, true>(),
+    entry<8, 64, 2, 256, true>(), entry<8, 32, 2, 256, true>(),
+    // the same with cached loads (weights re-read soon, e.g. warm caches)
+    entry<16, 32, 2, 256>(), entry<16, 32, 4, 256>(), entry<8, 64, 4, 256>(), entry<8, 32, 4, 256>(),
+    // full-column lane groups (measured slower; kept for comparison)
+    entry<16, 96, 2, 768>(), entry<8, 192, 4, 768>(),
+    // narrow tiles (decode latency)
+    entry<4, 64, 4, 256>(), entry<4, 16, 8, 256>(), entry<4, 16, 4, 1024>(), entry<4, 16, 16, 256>(),
+    entry<4, 8, 8, 1024>(), entry<4, 8, 16, 512>(), entry<8, 16, 8, 1024>(),
+    // any N, any alignment
+    entry<1, 64, 4, 256>(),
+};
+
+const ShapeEntry* find_shape(int code)
+{
+    for (const ShapeEntry& e : kShapes)
+        if (e.code == code)
+            return &e;
+    return nullptr;
+}
+
+int shape_tile(const ShapeEntry* e) { return e->vec * e->lanes; }
+
+// The shape's vector loads stay aligned and in range for this matrix.
+bool shape_fits(const ShapeEntry* e, const void* W, int64_t N)
 {
     const uintptr_t a = reinterpret_cast<uintptr_t>(W);
-    auto ok = [&](int v) { return N % v == 0 && a % v == 0; };
-    if (requested == 16 || requested == 8 || requested == 4 || requested == 1)
-        return ok(requested) ? requested : -1;
-    if (requested != 0)
-        return -1;
-    if (ok(16) && N % 512 == 0)
-        return SHAPE_V16_LG32;
-    if (ok(8))
-        return SHAPE_V8_LG64;
-    if (ok(4))
-        return SHAPE_V4_LG64;
-    return SHAPE_V1_LG64;
+    return N % e->vec == 0 && a % e->vec == 0;
 }
 
-constexpr int kMinTile = 64;  // smallest gather tile: sizes the counter array
+// Default throughput shape for a vector width (0: the widest that fits):
+// 512-byte tiles with nontemporal loads measured fastest on the 1536-wide
+// decode stack (and 16-byte lanes need N to be a multiple of 512 to keep
+// every lane busy).
+const ShapeEntry* default_shape(const void* W, int64_t N, int vec)
+{
+    static const int by_vec[][2] = {{16, SPIKE_SHAPE(16, 32, 2, 256) | SPIKE_SHAPE_NT},
+                                    {8, SPIKE_SHAPE(8, 64, 4, 256) | SPIKE_SHAPE_NT},
+                                    {4, SPIKE_SHAPE(4, 64, 4, 256)},
+                                    {1, SPIKE_SHAPE(1, 64, 4, 256)}};
+    for (const auto& bv : by_vec) {
+        if (vec != 0 && bv[0] != vec)
+            continue;
+        if (vec == 0 && bv[0] == 16 && N % 512 != 0)
+            continue;
+        const ShapeEntry* e = find_shape(bv[1]);
+        if (shape_fits(e, W, N))
+            return e;
+    }
+    return nullptr;
+}
+
+// Decode-latency shape for one or a few rows: no K-split (the atomic
+// epilogue costs three serialized memory round trips) and narrow tiles so
+// that enough workgroups share the active columns: 64-byte tiles for short
+// rows, 32-byte tiles with 1024-thread workgroups for long ones.
+const ShapeEntry* latency_shape(const void* W, int64_t N, int wpr)
+{
+    const int code = wpr <= 32 ? SPIKE_SHAPE(4, 16, 8, 256) : SPIKE_SHAPE(4, 8, 8, 1024);
+    const ShapeEntry* e = find_shape(code);
+    return shape_fits(e, W, N) ? e : nullptr;
+}
+
+constexpr int kMinTile = 32;  // smallest tile of any shape: sizes the counter array
 
 }  // namespace
 
@@ -81,27 +149,54 @@ struct spike_proj {
     int32_t K = 0, N = 0, wpr = 0;
     int device = 0;
     int32_t max_B = 0;
-    int32_t* ws = nullptr;          // [max_B][N] INT32, zero between calls
-    uint32_t* counters = nullptr;   // [max_B][counter_stride], zero between calls
+    int32_t* ws = nullptr;         // [max_B][N] INT32, zero between calls
+    uint32_t* counters = nullptr;  // [max_B][counter_stride], zero between calls
     int32_t counter_stride = 0;
     int path = SPIKE_PATH_AUTO;
-    int slice_words = 0;            // 0 = automatic
+    int slice_words = 0;  // 0 = automatic
     int max_slices = 16;
-    int vec_request = 0;            // 0 = automatic
-    int shape = SHAPE_V1_LG64;
+    const ShapeEntry* shape = nullptr;  // throughput shape (B above the latency range)
+    bool shape_pinned = false;          // set by SPIKE_TUNE_SHAPE / _VEC: used for every B
+    int tiles_per_unit = 1;
     int mfma_min_b = 64;
 };
 
 struct spike_stream {
     int32_t n_proj = 0, n_sets = 0, n_tokens = 0, N = 0;
-    int shape = SHAPE_V1_LG64;
+    const ShapeEntry* shape = nullptr;
+    int tiles_per_unit = 1;
+    int xcd_spread = 1;
     int max_wpr = 0;
     int device = 0;
     int64_t mask_stride = 0, out_stride = 0;
     spk::StreamDesc* d_desc = nullptr;
+    std::vector<const void*> weights;  // to re-check alignment when the shape changes
 };
 
 namespace {
+
+template <class S, bool ACC>
+void launch_gather_t(const spike_proj* h, const uint64_t* mask, int32_t B, int sw, int n_slices, int n_tiles,
+                     int tpu, float* out, int32_t* acc, hipStream_t st)
+{
+    const size_t dyn = spk::unit_dyn_lds<S>(sw, tpu);
+    const int64_t groups = (n_tiles + tpu - 1) / tpu;
+    const int64_t units = (int64_t)B * groups * n_slices;
+    hipLaunchKernelGGL((spk::k_gather<S, ACC>), dim3((unsigned)units), dim3(S::BLOCK), dyn, st, h->W, h->scale,
+                       h->K, h->N, mask, h->wpr, sw, n_slices, n_tiles, tpu, h->ws, h->counters, h->counter_stride,
+                       out, acc);
+}
+
+template <class S>
+void launch_stream_t(const spike_stream* s, int n_tiles, unsigned units, const uint64_t* masks, float* out,
+                     hipStream_t st)
+{
+    const size_t dyn = spk::unit_dyn_lds<S>(s->max_wpr, s->tiles_per_unit);
+    const int n_items = s->n_tokens * s->n_proj;
+    hipLaunchKernelGGL((spk::k_stream<S>), dim3(units), dim3(S::BLOCK), dyn, st, s->d_desc, s->n_proj, s->n_sets,
+                       s->N, n_tiles, s->tiles_per_unit, n_items, s->xcd_spread, masks, s->mask_stride, out,
+                       s->out_stride);
+}
 
 int alloc_workspace(spike_proj* h, int32_t max_B)
 {
@@ -150,57 +245,74 @@ int check_device(int want)
 // K-slices for a gather over B rows: enough units to spread one row over the
 // chip, capped so that the atomic traffic (slices * N * 4 bytes per row)
 // stays a small fraction of the weight bytes.
-int choose_slice_words(const spike_proj* h, int32_t B, int n_tiles)
+int choose_slice_words(const spike_proj* h, int32_t B, int n_groups)
 {
     int sw;
     if (h->slice_words > 0) {
         sw = h->slice_words;
     } else {
         const int64_t target_units = 2 * 256;
-        int64_t slices = (target_units + (int64_t)B * n_tiles - 1) / ((int64_t)B * n_tiles);
+        const int64_t per_slice = (int64_t)B * n_groups;
+        int64_t slices = (target_units + per_slice - 1) / per_slice;
         slices = std::max<int64_t>(1, std::min<int64_t>(slices, h->max_slices));
         sw = (int)((h->wpr + slices - 1) / slices);
     }
-    sw = std::max(1, std::min(sw, std::min(h->wpr, spk::kMaxSliceWords)));
-    return sw;
+    return std::max(1, std::min(sw, std::min(h->wpr, spk::kMaxSliceWords)));
 }
 
-template <int V, int LG, bool ACC>
-void launch_gather_t(const spike_proj* h, const uint64_t* mask, int32_t B, int sw, int n_slices, int n_tiles,
-                     float* out, int32_t* acc, hipStream_t st)
+// Launch plan of the gather for B rows: shape, mask words per K-slice and
+// tiles per workgroup.  Tuning knobs override the automatic choices.
+struct GatherPlan {
+    const ShapeEntry* shape;
+    int sw, n_slices, n_tiles, tpu;
+};
+
+constexpr int kLatencyRows = 4;  // up to this many rows use the decode-latency plan
+
+GatherPlan plan_gather(const spike_proj* h, int32_t B)
 {
-    const size_t dyn = spk::unit_dyn_lds<V, LG>(sw);
-    const int64_t units = (int64_t)B * n_tiles * n_slices;
-    hipLaunchKernelGGL((spk::k_gather<V, LG, ACC>), dim3((unsigned)units), dim3(spk::kBlock), dyn, st, h->W,
-                       h->scale, h->K, h->N, mask, h->wpr, sw, n_slices, n_tiles, h->ws, h->counters,
-                       h->counter_stride, out, acc);
+    GatherPlan p{};
+    p.shape = h->shape;
+    bool latency = false;
+    if (!h->shape_pinned && B <= kLatencyRows && h->wpr <= spk::kMaxSliceWords) {
+        if (const ShapeEntry* e = latency_shape(h->W, h->N, h->wpr)) {
+            p.shape = e;
+            latency = true;
+        }
+    }
+    const int tile = shape_tile(p.shape);
+    p.n_tiles = (int)((h->N + tile - 1) / tile);
+    p.tpu = std::min(h->tiles_per_unit, p.n_tiles);
+    const int n_groups = (p.n_tiles + p.tpu - 1) / p.tpu;
+    if (h->slice_words > 0)
+        p.sw = std::min(h->slice_words, std::min(h->wpr, spk::kMaxSliceWords));
+    else if (latency)
+        p.sw = h->wpr;
+    else
+        p.sw = choose_slice_words(h, B, n_groups);
+    p.n_slices = (int)((h->wpr + p.sw - 1) / p.sw);
+    return p;
 }
 
 template <bool ACC>
 int launch_gather(const spike_proj* h, const uint64_t* mask, int32_t B, float* out, int32_t* acc, hipStream_t st)
 {
-    const int n_tiles = (int)((h->N + shape_tile(h->shape) - 1) / shape_tile(h->shape));
-    const int sw = choose_slice_words(h, B, n_tiles);
-    const int n_slices = (int)((h->wpr + sw - 1) / sw);
-    const int64_t units = (int64_t)B * n_tiles * n_slices;
+    const GatherPlan p = plan_gather(h, B);
+    const int n_groups = (p.n_tiles + p.tpu - 1) / p.tpu;
+    const int64_t units = (int64_t)B * n_groups * p.n_slices;
     if (units > 0x7fffffff)
         return fail(SPIKE_EUNSUPPORTED, "launch of %lld workgroups is too large", (long long)units);
-    switch (h->shape) {
-    case SHAPE_V16_LG32: launch_gather_t<16, 32, ACC>(h, mask, B, sw, n_slices, n_tiles, out, acc, st); break;
-    case SHAPE_V8_LG64: launch_gather_t<8, 64, ACC>(h, mask, B, sw, n_slices, n_tiles, out, acc, st); break;
-    case SHAPE_V4_LG64: launch_gather_t<4, 64, ACC>(h, mask, B, sw, n_slices, n_tiles, out, acc, st); break;
-    default: launch_gather_t<1, 64, ACC>(h, mask, B, sw, n_slices, n_tiles, out, acc, st); break;
-    }
+    (ACC ? p.shape->gather_acc : p.shape->gather)(h, mask, B, p.sw, p.n_slices, p.n_tiles, p.tpu, out, acc, st);
     const hipError_t e = hipGetLastError();
     return e == hipSuccess ? SPIKE_OK : hip_fail(e, "gather launch");
 }
 
-int use_mfma(const spike_proj* h, int32_t B)
+bool use_mfma(const spike_proj* h, int32_t B)
 {
     if (h->path == SPIKE_PATH_MFMA)
-        return 1;
+        return true;
     if (h->path == SPIKE_PATH_GATHER)
-        return 0;
+        return false;
     return spk::mfma_supported(h->K, h->N, h->W) && B >= h->mfma_min_b;
 }
 
@@ -222,19 +334,24 @@ int forward_impl(spike_proj* h, const uint64_t* mask, int32_t B, float* out, int
         if (!spk::mfma_supported(h->K, h->N, h->W))
             return fail(SPIKE_EUNSUPPORTED, "matrix-core path needs N %% %d == 0 and a %d-byte aligned W",
                         spk::kMfmaNAlign, spk::kMfmaNAlign);
-        const hipError_t e = spk::launch_mfma(h->W, h->scale, h->K, h->N, mask, B, out, acc, ACC, st);
+        const hipError_t e = spk::launch_mfma(h->W, h->scale, h->K, h->N, mask, B, h->slice_words, h->ws,
+                                              h->counters, out, acc, ACC, st);
         return e == hipSuccess ? SPIKE_OK : hip_fail(e, "matrix-core launch");
     }
     return launch_gather<ACC>(h, mask, B, out, acc, st);
 }
 
-template <int V, int LG>
-void launch_stream_t(const spike_stream* s, int n_tiles, unsigned units, const uint64_t* masks, float* out,
-                     hipStream_t st)
+// Shape codes accepted by the tuning calls: 0 = automatic.
+int parse_shape(int value, const void* W, int64_t N, const ShapeEntry** out)
 {
-    const size_t dyn = spk::unit_dyn_lds<V, LG>(s->max_wpr);
-    hipLaunchKernelGGL((spk::k_stream<V, LG>), dim3(units), dim3(spk::kBlock), dyn, st, s->d_desc, s->n_proj, s->n_sets, s->N, n_tiles, masks, s->mask_stride, out,
-                       s->out_stride);
+    const ShapeEntry* e = value == 0 ? default_shape(W, N, 0) : find_shape(value);
+    if (!e)
+        return fail(SPIKE_EINVAL, "shape code 0x%x is not instantiated", value);
+    if (!shape_fits(e, W, N))
+        return fail(SPIKE_EINVAL, "shape with %d-byte loads does not fit N = %lld and the weight alignment", e->vec,
+                    (long long)N);
+    *out = e;
+    return SPIKE_OK;
 }
 
 }  // namespace
@@ -261,7 +378,7 @@ int spike_proj_create(const int8_t* W, const float* scale, int32_t K, int32_t N,
     h->K = K;
     h->N = N;
     h->wpr = (int32_t)words_per_row(K);
-    h->shape = pick_shape(W, N, 0);
+    h->shape = default_shape(W, N, 0);
     hipError_t e = hipGetDevice(&h->device);
     if (e != hipSuccess) {
         delete h;
@@ -340,17 +457,29 @@ int spike_proj_tune(spike_proj_t h, int32_t key, int32_t value)
         h->mfma_min_b = value;
         return SPIKE_OK;
     case SPIKE_TUNE_VEC: {
-        const int shape = pick_shape(h->W, h->N, value);
-        if (shape < 0)
+        if (value != 0 && value != 1 && value != 4 && value != 8 && value != 16)
+            return fail(SPIKE_EINVAL, "vector width %d is not 0, 1, 4, 8 or 16", value);
+        const ShapeEntry* e = default_shape(h->W, h->N, value);
+        if (!e)
             return fail(SPIKE_EINVAL, "vector width %d does not fit N = %d and the weight alignment", value, h->N);
-        h->vec_request = value;
-        h->shape = shape;
+        h->shape = e;
+        h->shape_pinned = value != 0;
         return SPIKE_OK;
     }
     case SPIKE_TUNE_MAX_SLICES:
         if (value < 1 || value > 4096)
             return fail(SPIKE_EINVAL, "max slices %d outside [1, 4096]", value);
         h->max_slices = value;
+        return SPIKE_OK;
+    case SPIKE_TUNE_SHAPE:
+        if (int rc = parse_shape(value, h->W, h->N, &h->shape))
+            return rc;
+        h->shape_pinned = value != 0;
+        return SPIKE_OK;
+    case SPIKE_TUNE_TILES_PER_UNIT:
+        if (value < 1 || value > 4096)
+            return fail(SPIKE_EINVAL, "tiles per unit %d outside [1, 4096]", value);
+        h->tiles_per_unit = value;
         return SPIKE_OK;
     default:
         return fail(SPIKE_EINVAL, "unknown tuning key %d", key);
@@ -367,10 +496,8 @@ int spike_compact(const uint64_t* mask, int32_t B, int32_t K, int32_t* active_id
         return SPIKE_OK;
     if (!mask || !active_idx || !active_count)
         return fail(SPIKE_EINVAL, "null pointer");
-    if (B > 0x7fffffff / 1)
-        return fail(SPIKE_EINVAL, "B too large");
-    hipLaunchKernelGGL(spk::k_compact, dim3((unsigned)B), dim3(spk::kBlock), 0, static_cast<hipStream_t>(stream),
-                       mask, K, (int)words_per_row(K), active_idx, active_count);
+    hipLaunchKernelGGL(spk::k_compact, dim3((unsigned)B), dim3(spk::kCompactBlock), 0,
+                       static_cast<hipStream_t>(stream), mask, K, (int)words_per_row(K), active_idx, active_count);
     const hipError_t e = hipGetLastError();
     return e == hipSuccess ? SPIKE_OK : hip_fail(e, "compaction launch");
 }
@@ -413,9 +540,11 @@ int spike_stream_create(const spike_proj_t* projs, int32_t n_proj, int32_t n_set
     if (!projs || n_proj < 1 || n_sets < 1 || n_tokens < 1)
         return fail(SPIKE_EINVAL, "n_proj, n_sets and n_tokens must be >= 1");
     const int64_t n_handles = (int64_t)n_proj * n_sets;
-    const int32_t N = projs[0] ? projs[0]->N : 0;
-    int shape = SHAPE_V16_LG32;
+    if (!projs[0])
+        return fail(SPIKE_EINVAL, "projection 0 is null");
+    const int32_t N = projs[0]->N;
     int max_wpr = 0;
+    std::vector<const void*> weights;
     for (int64_t i = 0; i < n_handles; ++i) {
         const spike_proj* p = projs[i];
         if (!p)
@@ -423,17 +552,31 @@ int spike_stream_create(const spike_proj_t* projs, int32_t n_proj, int32_t n_set
         if (p->N != N)
             return fail(SPIKE_EUNSUPPORTED, "all projections of a stream must share N (%d vs %d)", p->N, N);
         const spike_proj* first = projs[i % n_proj];
-        if (p->K != first->K)
-            return fail(SPIKE_EINVAL, "set %lld projection %lld has K = %d, set 0 has %d", (long long)(i / n_proj),
-                        (long long)(i % n_proj), p->K, first->K);
+        if (!first || p->K != first->K)
+            return fail(SPIKE_EINVAL, "set %lld projection %lld has a different K from set 0", (long long)(i / n_proj),
+                        (long long)(i % n_proj));
         if (p->wpr > spk::kMaxSliceWords)
             return fail(SPIKE_EUNSUPPORTED, "stream projections need K <= %d", 64 * spk::kMaxSliceWords);
-        shape = std::min(shape, pick_shape(p->W, N, 0));
         max_wpr = std::max(max_wpr, p->wpr);
+        weights.push_back(p->W);
+    }
+    // the widest default shape whose loads fit every weight matrix
+    const ShapeEntry* shape = nullptr;
+    for (int vec : {16, 8, 4, 1}) {
+        const ShapeEntry* e = default_shape(weights[0], N, vec);
+        if (!e || (vec == 16 && N % 512 != 0))
+            continue;
+        bool ok = true;
+        for (const void* w : weights)
+            ok = ok && shape_fits(e, w, N);
+        if (ok) {
+            shape = e;
+            break;
+        }
     }
     const int tile = shape_tile(shape);
     const int64_t n_tiles = (N + tile - 1) / tile;
-    if ((int64_t)n_tokens * n_proj * n_tiles > 0x7fffffff)
+    if (((int64_t)n_tokens * n_proj + 8) * n_tiles > 0x7fffffff)
         return fail(SPIKE_EUNSUPPORTED, "stream of %d tokens is too large for one launch", n_tokens);
     std::vector<spk::StreamDesc> desc((size_t)n_handles);
     int64_t moff = 0;
@@ -461,6 +604,7 @@ int spike_stream_create(const spike_proj_t* projs, int32_t n_proj, int32_t n_set
     s->max_wpr = max_wpr;
     s->mask_stride = moff;
     s->out_stride = (int64_t)n_proj * N;
+    s->weights = std::move(weights);
     hipError_t e = hipGetDevice(&s->device);
     if (e == hipSuccess)
         e = hipMalloc(&s->d_desc, desc.size() * sizeof(spk::StreamDesc));
@@ -476,6 +620,38 @@ int spike_stream_create(const spike_proj_t* projs, int32_t n_proj, int32_t n_set
     return SPIKE_OK;
 }
 
+int spike_stream_tune(spike_stream_t s, int32_t key, int32_t value)
+{
+    g_last_error.clear();
+    if (!s)
+        return fail(SPIKE_EINVAL, "null stream handle");
+    switch (key) {
+    case SPIKE_TUNE_SHAPE: {
+        const ShapeEntry* e = nullptr;
+        for (const void* w : s->weights)
+            if (int rc = parse_shape(value, w, s->N, &e))
+                return rc;
+        const int64_t n_tiles = (s->N + shape_tile(e) - 1) / shape_tile(e);
+        if (((int64_t)s->n_tokens * s->n_proj + 8) * n_tiles > 0x7fffffff)
+            return fail(SPIKE_EUNSUPPORTED, "shape makes the launch too large");
+        s->shape = e;
+        return SPIKE_OK;
+    }
+    case SPIKE_TUNE_TILES_PER_UNIT:
+        if (value < 1 || value > 4096)
+            return fail(SPIKE_EINVAL, "tiles per unit %d outside [1, 4096]", value);
+        s->tiles_per_unit = value;
+        return SPIKE_OK;
+    case SPIKE_TUNE_XCD_SPREAD:
+        if (value != 1 && value != 8)
+            return fail(SPIKE_EINVAL, "xcd spread must be 1 or 8, got %d", value);
+        s->xcd_spread = value;
+        return SPIKE_OK;
+    default:
+        return fail(SPIKE_EINVAL, "key %d does not apply to a stream", key);
+    }
+}
+
 int spike_stream_forward(spike_stream_t s, const uint64_t* masks, float* out, void* stream)
 {
     g_last_error.clear();
@@ -487,14 +663,15 @@ int spike_stream_forward(spike_stream_t s, const uint64_t* masks, float* out, vo
         return rc;
     const int tile = shape_tile(s->shape);
     const int n_tiles = (s->N + tile - 1) / tile;
-    const unsigned units = (unsigned)((int64_t)s->n_tokens * s->n_proj * n_tiles);
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    switch (s->shape) {
-    case SHAPE_V16_LG32: launch_stream_t<16, 32>(s, n_tiles, units, masks, out, st); break;
-    case SHAPE_V8_LG64: launch_stream_t<8, 64>(s, n_tiles, units, masks, out, st); break;
-    case SHAPE_V4_LG64: launch_stream_t<4, 64>(s, n_tiles, units, masks, out, st); break;
-    default: launch_stream_t<1, 64>(s, n_tiles, units, masks, out, st); break;
-    }
+    const int tpu = std::min(s->tiles_per_unit, n_tiles);
+    const int n_groups = (n_tiles + tpu - 1) / tpu;
+    const int64_t n_items = (int64_t)s->n_tokens * s->n_proj;
+    const int64_t padded = (n_items + s->xcd_spread - 1) / s->xcd_spread * s->xcd_spread;
+    const unsigned units = (unsigned)(padded * n_groups);
+    const int saved = s->tiles_per_unit;
+    s->tiles_per_unit = tpu;  // launch with the clamped value
+    s->shape->stream(s, n_tiles, units, masks, out, static_cast<hipStream_t>(stream));
+    s->tiles_per_unit = saved;
     const hipError_t e = hipGetLastError();
     return e == hipSuccess ? SPIKE_OK : hip_fail(e, "stream launch");
 }
@@ -511,6 +688,14 @@ int spike_stream_destroy(spike_stream_t s)
         (void)hipFree(s->d_desc);
     delete s;
     return rc;
+}
+
+int spike_proj_shapes(int32_t* codes, int32_t cap)
+{
+    const int n = (int)(sizeof kShapes / sizeof kShapes[0]);
+    for (int i = 0; i < n && i < cap && codes; ++i)
+        codes[i] = kShapes[i].code;
+    return n;
 }
 
 const char* spike_proj_last_error(void) { return g_last_error.c_str(); }

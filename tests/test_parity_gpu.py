@@ -425,3 +425,109 @@ def test_errors_on_gpu(sp):
     with pytest.raises(sp.SpikeError) as e:
         sp.spike_stream_create([h, h2], 2, 1, 4)
     assert e.value.code == sp.SPIKE_EUNSUPPORTED
+
+
+def decode_shape(code):
+    return dict(V=code & 31, LG=(code >> 5) & 1023, U=(code >> 15) & 31, BLOCK=((code >> 20) & 31) * 64,
+                NT=bool(code >> 25 & 1))
+
+
+@pytest.mark.parametrize("K,N", [(1536, 1536), (6144, 1536), (333, 1000), (70, 96)])
+def test_every_instantiated_shape(sp, K, N):
+    """Every launch shape the library instantiates, with and without K-slices
+    and with several tiles per workgroup, gives the oracle's bits."""
+    p = wl.small_problem(K, N, 3, 0.2, seed=K ^ N)
+    h, *_ = make(sp, p["W"], p["scale"])
+    wpr = wl.words_per_row(K)
+    ran = 0
+    for code in sp.spike_proj_shapes():
+        try:
+            sp.spike_proj_tune(h, sp.SPIKE_TUNE_SHAPE, code)
+        except sp.SpikeError:
+            assert N % decode_shape(code)["V"] != 0  # only a misfit vector width may be refused
+            continue
+        for sw, tpu in ((wpr, 1), (max(1, wpr // 3), 1), (1, 3)):
+            sp.spike_proj_tune(h, sp.SPIKE_TUNE_SLICE_WORDS, min(sw, 256))
+            sp.spike_proj_tune(h, sp.SPIKE_TUNE_TILES_PER_UNIT, tpu)
+            assert_parity(sp, h, p["W"], p["scale"], p["masks"])
+        ran += 1
+    assert ran >= 10
+
+
+def test_stream_every_shape_and_xcd_spread(sp, stack):
+    hs, host = stack
+    T = 3
+    masks = wl.stack_token_masks(T)
+    st = sp.spike_stream_create(hs, 44, 1, T)
+    ref = torch.full((T, 44 * 1536), float("nan"), device="cuda")
+    sp.spike_stream_forward(st, dmask(masks), ref)
+    torch.cuda.synchronize()
+    got_ref = ref.cpu().numpy()
+    moff = 0
+    for j, (W, s) in enumerate(host):  # the default shape against the oracle
+        wpr = wl.words_per_row(W.shape[0])
+        np.testing.assert_array_equal(bits32(got_ref[1, j * 1536:(j + 1) * 1536]),
+                                      bits32(oracle.spike_forward(W, s, masks[1:2, moff:moff + wpr])[0]))
+        moff += wpr
+    for code in sp.spike_proj_shapes():
+        for tpu in (1, 2):
+            for spread in (1, 8):
+                sp.spike_stream_tune(st, sp.SPIKE_TUNE_SHAPE, code)
+                sp.spike_stream_tune(st, sp.SPIKE_TUNE_TILES_PER_UNIT, tpu)
+                sp.spike_stream_tune(st, sp.SPIKE_TUNE_XCD_SPREAD, spread)
+                out = torch.full_like(ref, float("nan"))
+                sp.spike_stream_forward(st, dmask(masks), out)
+                torch.cuda.synchronize()
+                assert torch.equal(out.view(torch.int32), ref.view(torch.int32)), (hex(code), tpu, spread)
+
+
+@pytest.mark.parametrize("B", [1, 17, 64, 65, 130])
+@pytest.mark.parametrize("K,N", [(100, 64), (1536, 1536), (4097, 192), (6144, 1024)])
+def test_matrix_core_path(sp, B, K, N):
+    """The dense i8 matrix-core contraction over the 0/1 spike matrix gives the
+    oracle's bits, with and without K-splits, for ragged B and K."""
+    p = wl.small_problem(K, N, B, 0.15, seed=B * 7 + K)
+    h, *_ = make(sp, p["W"], p["scale"])
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
+    wpr = wl.words_per_row(K)
+    for wps in (0, 1, 3, wpr):
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_SLICE_WORDS, min(wps, 256))
+        assert_parity(sp, h, p["W"], p["scale"], p["masks"])
+
+
+def test_matrix_core_extremes(sp):
+    K, N = 2048, 128
+    W = np.full((K, N), -128, np.int8)
+    W[:, ::3] = 127
+    scale = np.full(N, 2.0 ** -140, np.float32)
+    scale[1::4] = 1e-2
+    bits = np.ones((70, K), bool)
+    bits[3] = False
+    masks = wl.pack_bits(bits)
+    masks[:, -1] |= np.uint64(0)  # K is a multiple of 64: no padding bits
+    h, *_ = make(sp, W, scale)
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
+    assert_parity(sp, h, W, scale, masks)
+
+
+def test_matrix_core_rejects_unaligned_N(sp):
+    p = wl.small_problem(128, 100, 4, 0.3)
+    h, *_ = make(sp, p["W"], p["scale"])
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
+    out = torch.empty((4, 100), device="cuda")
+    with pytest.raises(sp.SpikeError) as e:
+        sp.spike_proj_forward(h, dmask(p["masks"]), 4, out)
+    assert e.value.code == sp.SPIKE_EUNSUPPORTED
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_AUTO)  # AUTO falls back to the gather
+    assert_parity(sp, h, p["W"], p["scale"], p["masks"])
+
+
+def test_paths_agree_on_prefill_and_padding_junk(sp):
+    d = wl.prefill_projection(B=200)
+    masks = d["masks"].copy()
+    h, *_ = make(sp, d["W"], d["scale"])
+    outs = {}
+    for path in (sp.SPIKE_PATH_GATHER, sp.SPIKE_PATH_MFMA):
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, path)
+        outs[path] = bits32(gpu_forward(sp, h, masks))
+    np.testing.assert_array_equal(outs[sp.SPIKE_PATH_GATHER], outs[sp.SPIKE_PATH_MFMA])
