@@ -1,9 +1,9 @@
 """Benchmark of the spike-gated INT8 projection on one MI355X.
 
-Workload (default): the 22-block decode stack of the 874M spiking decoder --
+Headline workload: the 22-block decode stack of the 874M spiking decoder --
 per block a TCAM projection 1536 -> 1536 and an FFN down projection
-6144 -> 1536, per-block spike rate r_l ~ U[0.05, 0.20], 1000 tokens of
-fresh Bernoulli spikes, independent INT8 weights per projection (~260 MB).
+6144 -> 1536, per-block spike rate r_l ~ U[0.05, 0.20], 1000 tokens of fresh
+Bernoulli spikes, independent INT8 weights per projection (~260 MB).
 
 A step is one pass of the whole 1000-token stream through all 44
 projections: one launch of the stream kernel, in which every (token,
@@ -18,11 +18,14 @@ Headline value: active-column INT8 bytes per second (sum over tokens and
 projections of |A| * N bytes, the only weight bytes the method needs),
 against the MI355X HBM peak of 8 TB/s.  Also reported: the per-token
 latency of the 44 projections run in stream order (graph replay, median and
-p99), and the CPU oracle on a bounded sample of the same workload.
+p99); the single projection and the down-projection rate sweep at batch 1;
+the 512-token prefill on the gather and on the matrix cores; the batched
+decode stack (64 rows); and the CPU oracle on a bounded sample.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -35,26 +38,79 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, published
-DEFAULT_SETS = 32          # rotated weight copies (8.3 GB)
+INT8_PEAK_TOPS = 5000.0    # MI355X dense int8 matrix peak, published
+DEFAULT_SETS = 32          # rotated weight copies of the decode stack (8.3 GB)
 DEFAULT_TOKENS = 1000
 METRIC = "active-column INT8 GB/s (% HBM peak) + per-token 22-layer spike-proj latency"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_stream_decode_stack_traffic.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_03026_amd", "csrc", f) for f in ("gather.hpp", "spike_proj.hip")]
 
 
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def active_bytes(masks: np.ndarray, Ks, N: int) -> np.ndarray:
-    """|A| * N per (token, projection) from the packed masks."""
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def active_counts(masks: np.ndarray, Ks) -> np.ndarray:
+    """|A| per (row, projection) from masks packed projection after projection."""
     from paper_2606_03026_amd import workloads as wl
     out = np.empty((masks.shape[0], len(Ks)), dtype=np.int64)
     off = 0
     for j, K in enumerate(Ks):
         w = wl.words_per_row(K)
-        bits = wl.unpack_bits(masks[:, off:off + w], K)
-        out[:, j] = bits.sum(axis=1) * N
+        out[:, j] = wl.unpack_bits(masks[:, off:off + w], K).sum(axis=1)
         off += w
     return out
+
+
+class Timer:
+    """HIP events on torch's current stream, which is the stream every
+    binding call launches on."""
+
+    def __init__(self, torch):
+        self.torch = torch
+
+    def __call__(self, fn, reps: int, warmup: int = 1) -> float:
+        torch = self.torch
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / 1e3 / reps
+
+
+def graph_of(torch, fn):
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    return g
+
+
+def make_handles(sp, torch, host, copies: int):
+    """Device weights and handles for (W, scale) pairs, plus `copies` - 1
+    address-distinct device copies of all of them."""
+    dev = [(torch.from_numpy(W).cuda(), torch.from_numpy(s).cuda()) for (W, s) in host]
+    base = [sp.spike_proj_create(W, s) for (W, s) in dev]
+    extra = []
+    for _ in range(copies - 1):
+        for (W, s) in dev:
+            h = sp.spike_proj_create(W.clone(), s.clone())
+            sp.spike_proj_reserve(h, 1)
+            extra.append(h)
+    return base, extra
 
 
 def cpu_baseline(host, masks, Ks, budget_s: float, threads: int):
@@ -75,6 +131,154 @@ def cpu_baseline(host, masks, Ks, budget_s: float, threads: int):
     return done_bytes / el / 1e9, tokens, el
 
 
+def bench_decode_stack(sp, torch, wl, timer, args):
+    T, R = args.tokens, args.sets
+    order = wl.stack_order()
+    Ks = [wl.PROJ_SHAPES[j][0] for (_, j) in order]
+    N = wl.RESIDUAL
+    log(f"decode stack: weights for {len(order)} projections, {T} tokens of spikes, {R} weight sets")
+    host = [wl.stack_projection(l, j) for (l, j) in order]
+    masks = wl.stack_token_masks(T)
+    counts = active_counts(masks, Ks)
+    step_bytes = int(counts.sum()) * N
+    handles, copies = make_handles(sp, torch, host, R)
+    dmasks = torch.from_numpy(masks.view(np.int64)).cuda()
+    out = torch.empty((T, len(order) * N), dtype=torch.float32, device="cuda")
+    cold = sp.spike_stream_create(handles + copies, len(order), R, T)
+    warm = sp.spike_stream_create(handles, len(order), 1, T)
+    torch.cuda.synchronize()
+
+    sec = timer(lambda: sp.spike_stream_forward(cold, dmasks, out), args.steps, args.warmup)
+    gbs = step_bytes / sec / 1e9
+    log(f"stream cold: {sec * 1e3:.3f} ms/step, {gbs:.1f} GB/s active-column ({100 * gbs / HBM_PEAK_GBS:.1f}% of HBM)")
+    sec_w = timer(lambda: sp.spike_stream_forward(warm, dmasks, out), max(3, args.steps // 2), 1)
+    warm_gbs = step_bytes / sec_w / 1e9
+    log(f"stream warm: {warm_gbs:.1f} GB/s")
+    res = {"sec": sec, "gbs": gbs, "warm_gbs": warm_gbs, "step_bytes": step_bytes, "host": host, "masks": masks,
+           "Ks": Ks}
+
+    if not args.no_latency:
+        static_mask = torch.zeros(masks.shape[1], dtype=torch.int64, device="cuda")
+        static_out = torch.zeros(len(order) * N, device="cuda")
+        g = graph_of(torch, lambda: sp.spike_stack_forward(handles, static_mask, 1, static_out))
+        nt = min(args.latency_tokens, T)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(nt)]
+        # Keep the device behind the host: a spin kernel at the head of every
+        # chunk covers the time the host needs to enqueue the chunk, so no
+        # token's start event can run ahead of its graph launch.
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        torch.cuda._sleep(1_000_000)
+        b.record()
+        torch.cuda.synchronize()
+        cycles_per_ms = 1_000_000 / max(a.elapsed_time(b), 1e-3)
+        for c0 in range(0, nt, 50):
+            torch.cuda._sleep(int(cycles_per_ms * 30))
+            for t in range(c0, min(nt, c0 + 50)):
+                static_mask.copy_(dmasks[t])
+                evs[t][0].record()
+                g.replay()
+                evs[t][1].record()
+        torch.cuda.synchronize()
+        skip = min(10, nt - 1)
+        lat = np.array([x.elapsed_time(y) * 1e3 for x, y in evs])[skip:]
+        tok_bytes = counts[:nt].sum(axis=1)[skip:] * N
+        res["latency"] = {"median_us": round(float(np.median(lat)), 2),
+                          "p99_us": round(float(np.percentile(lat, 99)), 2), "tokens": int(lat.size),
+                          "gbs_median": round(float(np.median(tok_bytes / lat / 1e3)), 1),
+                          "mode": "44 batch-1 projections in stream order per token (HIP graph replay), "
+                                  "warm weights"}
+        log(f"per-token latency: median {res['latency']['median_us']} us, p99 {res['latency']['p99_us']} us")
+    for s in (cold, warm):
+        s.close()
+    return res
+
+
+def bench_batch1(sp, torch, wl, timer, name, d, sets: int, calls: int):
+    """One projection at batch 1: mean latency of `calls` dependent calls
+    (graph replay) and the stream rate over the same masks on `sets` rotated
+    weight copies."""
+    K, N = d["K"], d["N"]
+    masks = d["masks"]
+    nm = masks.shape[0]
+    counts = active_counts(masks, [K])[:, 0]
+    handles, copies = make_handles(sp, torch, [(d["W"], d["scale"])], sets)
+    h = handles[0]
+    dm = torch.from_numpy(masks.view(np.int64)).cuda()
+    out = torch.empty((nm, N), device="cuda")
+    n = min(calls, nm)
+    g = graph_of(torch, lambda: [sp.spike_proj_forward(h, dm[i], 1, out[i]) for i in range(n)])
+    sec = timer(g.replay, 3, 1) / n
+    st = sp.spike_stream_create(handles + copies, 1, sets, nm)
+    sec_s = timer(lambda: sp.spike_stream_forward(st, dm, out), 5, 1)
+    st.close()
+    bytes_per = float(counts.mean()) * N
+    r = {"K": K, "N": N, "p": d["p"], "active_bytes_mean": round(bytes_per), "call_us": round(sec * 1e6, 2),
+         "call_gbs": round(bytes_per / sec / 1e9, 1), "stream_gbs": round(counts.sum() * N / sec_s / 1e9, 1),
+         "stream_sets": sets, "masks": nm}
+    log(f"{name}: {r['call_us']} us per dependent call ({r['call_gbs']} GB/s); stream {r['stream_gbs']} GB/s")
+    return r
+
+
+def bench_prefill(sp, torch, wl, timer):
+    d = wl.prefill_projection()
+    B, K, N = d["masks"].shape[0], d["K"], d["N"]
+    h = make_handles(sp, torch, [(d["W"], d["scale"])], 1)[0][0]
+    dm = torch.from_numpy(d["masks"].view(np.int64)).cuda()
+    out = torch.empty((B, N), device="cuda")
+    r = {"B": B, "K": K, "N": N}
+    for name, path in (("gather", sp.SPIKE_PATH_GATHER), ("mfma", sp.SPIKE_PATH_MFMA)):
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, path)
+        sec = timer(lambda: sp.spike_proj_forward(h, dm, B, out), 20, 2)
+        r[f"{name}_us"] = round(sec * 1e6, 2)
+    ops = 2.0 * B * K * N
+    r["mfma_tops"] = round(ops / (r["mfma_us"] * 1e-6) / 1e12, 1)
+    r["mfma_util"] = round(r["mfma_tops"] / INT8_PEAK_TOPS, 4)
+    r["speedup_mfma_vs_gather"] = round(r["gather_us"] / r["mfma_us"], 2)
+    log(f"prefill 512x6144->1536: gather {r['gather_us']} us, matrix cores {r['mfma_us']} us "
+        f"({r['mfma_tops']} TOPS dense, {100 * r['mfma_util']:.1f}% of int8 peak)")
+    return r
+
+
+def bench_batched_stack(sp, torch, wl, timer, steps: int = 16, B: int = 64):
+    order = wl.stack_order()
+    host = [wl.batched_stack_projection(l, j) for (l, j) in order]
+    bits = [wl.batched_stack_bits(l, j, B=B, n_steps=steps) for (l, j) in order]
+    handles = make_handles(sp, torch, host, 1)[0]
+    per_step = [np.concatenate([wl.pack_bits(b[s]).reshape(-1) for b in bits]) for s in range(steps)]
+    union = sum(int(b.any(axis=1).sum(axis=1).mean()) * 1536 for b in bits)  # mean union columns per step
+    dm = [torch.from_numpy(m.view(np.int64)).cuda() for m in per_step]
+    static = torch.zeros_like(dm[0])
+    out = torch.empty(sum(B * h.N for h in handles), device="cuda")
+    r = {"B": B, "steps": steps, "union_bytes_per_step": union}
+    for name, path in (("mfma", sp.SPIKE_PATH_AUTO), ("gather", sp.SPIKE_PATH_GATHER)):
+        for h in handles:
+            sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, path)
+        g = graph_of(torch, lambda: sp.spike_stack_forward(handles, static, B, out))
+        times = []
+        for s in range(steps):
+            static.copy_(dm[s])
+            times.append(timer(g.replay, 1, 0))
+        t = float(np.median(times))
+        r[f"{name}_step_us"] = round(t * 1e6, 1)
+        r[f"{name}_union_gbs"] = round(union / t / 1e9, 1)
+    log(f"batched stack B={B}: matrix cores {r['mfma_step_us']} us/step ({r['mfma_union_gbs']} GB/s on union "
+        f"bytes), gather {r['gather_step_us']} us/step")
+    return r
+
+
+def traffic_record():
+    """HBM bytes per stream launch from the committed rocprofv3 PMC summary,
+    if it was taken on the current kernel sources."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return rec
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -86,6 +290,9 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-budget", type=float, default=8.0, help="seconds per CPU-baseline leg")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-latency", action="store_true")
+    ap.add_argument("--only-stream", action="store_true", help="time only the headline stream (for profiling)")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run a 1 GiB device copy first (reference for the PMC byte counters)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -99,101 +306,45 @@ def main(argv=None) -> int:
     from paper_2606_03026_amd import workloads as wl
 
     torch.cuda.set_device(0)
-    T, R = args.tokens, args.sets
-    order = wl.stack_order()
-    Ks = [wl.PROJ_SHAPES[j][0] for (_, j) in order]
-    N = wl.RESIDUAL
-
-    log(f"generating weights for {len(order)} projections and {T} tokens of spikes")
-    host = [wl.stack_projection(l, j) for (l, j) in order]
-    masks = wl.stack_token_masks(T)
-    ab = active_bytes(masks, Ks, N)
-    step_bytes = int(ab.sum())
-
-    dev_w = [(torch.from_numpy(W).cuda(), torch.from_numpy(s).cuda()) for (W, s) in host]
-    handles = [sp.spike_proj_create(W, s) for (W, s) in dev_w]
-    copies = []
-    for _ in range(R - 1):
-        for (W, s) in dev_w:
-            Wc, sc = W.clone(), s.clone()
-            h = sp.spike_proj_create(Wc, sc)
-            sp.spike_proj_reserve(h, 1)
-            copies.append(h)
-    dmasks = torch.from_numpy(masks.view(np.int64)).cuda()
-    out = torch.empty((T, len(order) * N), dtype=torch.float32, device="cuda")
-    stream_cold = sp.spike_stream_create(handles + copies, len(order), R, T)
-    stream_warm = sp.spike_stream_create(handles, len(order), 1, T)
-    torch.cuda.synchronize()
-    log(f"weights resident: {R} sets x {sum(W.numel() for W, _ in dev_w) / 1e6:.1f} MB; "
-        f"active bytes per step {step_bytes / 1e9:.3f} GB")
-
-    def timed(stream_handle, steps, warmup):
-        for _ in range(warmup):
-            sp.spike_stream_forward(stream_handle, dmasks, out)
+    timer = Timer(torch)
+    if args.copy_probe:
+        src = torch.ones(1 << 28, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
         torch.cuda.synchronize()
-        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        start.record()
-        for _ in range(steps):
-            sp.spike_stream_forward(stream_handle, dmasks, out)
-        end.record()
-        torch.cuda.synchronize()
-        return start.elapsed_time(end) / 1e3
+        log("copy probe: 1 GiB read + 1 GiB written")
+        del src, dst
 
-    el = timed(stream_cold, args.steps, args.warmup)
-    ms_per_step = el / args.steps * 1e3
-    gbs = step_bytes * args.steps / el / 1e9
-    log(f"stream (cold, {R} sets): {ms_per_step:.3f} ms/step, {gbs:.1f} GB/s active-column")
-    el_w = timed(stream_warm, max(3, args.steps // 2), 1)
-    warm_gbs = step_bytes * max(3, args.steps // 2) / el_w / 1e9
-    log(f"stream (warm, 1 set): {warm_gbs:.1f} GB/s")
+    if args.only_stream:
+        args.no_latency = True
+    main_res = bench_decode_stack(sp, torch, wl, timer, args)
+    gbs = main_res["gbs"]
 
-    latency = None
-    if not args.no_latency:
-        words = masks.shape[1]
-        static_mask = torch.zeros(words, dtype=torch.int64, device="cuda")
-        static_out = torch.zeros(len(order) * N, device="cuda")
-        sp.spike_stack_forward(handles, static_mask, 1, static_out)
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            sp.spike_stack_forward(handles, static_mask, 1, static_out)
-        nt = min(args.latency_tokens, T)
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(nt)]
-        # Keep the device behind the host: a spin kernel at the head of every
-        # chunk covers the time the host needs to enqueue the chunk, so no
-        # token's start event can run ahead of its graph launch.
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        torch.cuda._sleep(1_000_000)
-        b.record()
-        torch.cuda.synchronize()
-        cycles_per_ms = 1_000_000 / max(a.elapsed_time(b), 1e-3)
-        chunk = 50
-        for c0 in range(0, nt, chunk):
-            torch.cuda._sleep(int(cycles_per_ms * 30))
-            for t in range(c0, min(nt, c0 + chunk)):
-                static_mask.copy_(dmasks[t])
-                evs[t][0].record()
-                g.replay()
-                evs[t][1].record()
-        torch.cuda.synchronize()
-        lat = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])[min(10, nt - 1):]
-        lat_bytes = ab[:nt].sum(axis=1)[min(10, nt - 1):]
-        latency = {"median_us": round(float(np.median(lat)), 2), "p99_us": round(float(np.percentile(lat, 99)), 2),
-                   "tokens": int(lat.size), "gbs_median": round(float(np.median(lat_bytes / lat / 1e3)), 1),
-                   "mode": "44 projections in stream order per token, graph replay, warm weights"}
-        log(f"per-token latency: median {latency['median_us']} us, p99 {latency['p99_us']} us")
+    extra = {}
+    if not args.only_stream:
+        extra["single_1536x1536_b1"] = bench_batch1(sp, torch, wl, timer, "1536x1536 p=0.10",
+                                                    wl.single_projection(n_masks=1000), 32, 1000)
+        extra["down_6144x1536_b1"] = [
+            bench_batch1(sp, torch, wl, timer, f"6144x1536 p={p}", wl.down_sweep(p, n_masks=1000), 32, 200)
+            for p in wl.DOWN_SWEEP_RATES]
+        extra["prefill_512x6144x1536"] = bench_prefill(sp, torch, wl, timer)
+        extra["batched_stack_b64"] = bench_batched_stack(sp, torch, wl, timer)
 
     cpu = None
     if not args.no_cpu:
         cores = min(len(os.sched_getaffinity(0)), 16)
+        host, masks, Ks = main_res["host"], main_res["masks"], main_res["Ks"]
         v1, tok1, el1 = cpu_baseline(host, masks, Ks, args.cpu_budget, 1)
         vn, tokn, eln = cpu_baseline(host, masks, Ks, args.cpu_budget, cores)
-        cpu = {"value": round(vn, 3), "unit": "GB/s", "cores": cores, "kind": "oracle",
-               "sample": f"first {tokn} tokens x 44 projections of the same stream ({eln:.1f} s)",
-               "single_thread": {"value": round(v1, 3), "sample_tokens": tok1, "seconds": round(el1, 1)}}
-        log(f"cpu oracle: {v1:.2f} GB/s on 1 thread, {vn:.2f} GB/s on {cores}")
+        best_multi = vn >= v1
+        cpu = {"value": round(max(v1, vn), 3), "unit": "GB/s", "cores": cores if best_multi else 1,
+               "kind": "oracle",
+               "sample": (f"first {tokn if best_multi else tok1} tokens x 44 projections of the same stream "
+                          f"({eln if best_multi else el1:.1f} s); 1 thread: {v1:.3f} GB/s over {tok1} tokens, "
+                          f"{cores} threads: {vn:.3f} GB/s over {tokn} tokens")}
+        log(f"cpu oracle: {v1:.3f} GB/s on 1 thread, {vn:.3f} GB/s on {cores}")
 
+    traffic = traffic_record()
     rec = {
         "metric": METRIC,
         "value": round(gbs, 1),
@@ -201,28 +352,28 @@ def main(argv=None) -> int:
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": round(main_res["sec"] * 1e3, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "int8",
         "data": "synthetic",
         "config": {"workload": "22-block decode stack, TCAM 1536->1536 + FFN down 6144->1536 per block, "
-                               f"batch-1 per token, {T} tokens, rate U[0.05,0.20] per block, "
-                               f"independent-token stream over {R} rotated weight copies",
-                   "tokens": T, "projections_per_token": len(order), "weight_sets": R,
-                   "active_bytes_per_step": step_bytes},
+                               f"batch-1 per token, {args.tokens} tokens, rate U[0.05,0.20] per block, "
+                               f"independent-token stream over {args.sets} rotated weight copies",
+                   "tokens": args.tokens, "projections_per_token": 44, "weight_sets": args.sets,
+                   "active_bytes_per_step": main_res["step_bytes"]},
         "hbm_pct": round(100 * gbs / HBM_PEAK_GBS, 2),
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "k_stream (one launch per step)"},
-        "warm_gbs": round(warm_gbs, 1),
-        "per_token_latency": latency,
+                     "frac": round(gbs / HBM_PEAK_GBS, 4),
+                     "traffic": None if traffic is None else traffic["hbm_bytes_per_launch"],
+                     "kernel": "k_stream (one launch per step)", "kernel_source_hash": kernel_source_hash()},
+        "warm_gbs": round(main_res["warm_gbs"], 1),
+        "per_token_latency": main_res.get("latency"),
+        "workloads": extra,
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
-    for s in (stream_cold, stream_warm):
-        s.close()
     return 0
 
 

@@ -109,6 +109,12 @@ int spike_proj_destroy(spike_proj_t h);
  *                           (1..4096); the active list is built once per unit
  *   SPIKE_TUNE_XCD_SPREAD   streams only: 1 = plain unit order; 8 = keep the
  *                           tiles of one (token, projection) on one XCD
+ *   SPIKE_TUNE_MFMA_WAVES   waves per workgroup of the matrix-core path, which
+ *                           share one tile's K range: 0 = automatic, 4, 8
+ *   SPIKE_TUNE_MFMA_SPLIT_WORDS  mask words per K-split of the matrix-core
+ *                           path (0 = automatic).  Splits exist only for
+ *                           B <= 64 and at most 8 of them; a forward that
+ *                           would need more returns SPIKE_EUNSUPPORTED.
  * Returns SPIKE_EINVAL for an unknown key or a value out of range.
  */
 #define SPIKE_TUNE_PATH 1
@@ -119,6 +125,8 @@ int spike_proj_destroy(spike_proj_t h);
 #define SPIKE_TUNE_SHAPE 6
 #define SPIKE_TUNE_TILES_PER_UNIT 7
 #define SPIKE_TUNE_XCD_SPREAD 8
+#define SPIKE_TUNE_MFMA_WAVES 9
+#define SPIKE_TUNE_MFMA_SPLIT_WORDS 10
 #define SPIKE_SHAPE(V, LG, U, BLOCK) ((V) | ((LG) << 5) | ((U) << 15) | (((BLOCK) / 64) << 20))
 #define SPIKE_SHAPE_NT (1 << 25) /* or-ed into a shape code: nontemporal weight loads */
 #define SPIKE_PATH_AUTO 0

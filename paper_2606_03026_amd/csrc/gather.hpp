@@ -104,6 +104,18 @@ __device__ inline int compact_slice(const uint64_t* __restrict__ row, int w0, in
     return total;
 }
 
+// Cross-workgroup hand-off without cache maintenance.  A device-scope
+// release/acquire fence on this chip writes back and invalidates the whole
+// L2 of the XCD (buffer_wbl2 / buffer_inv), which stalls every workgroup that
+// shares it.  The split-K hand-offs here need none of that: every datum that
+// crosses workgroups is written and read with device-coherent operations
+// (INT32 atomics, or atomic stores/loads of device scope, which bypass the
+// non-coherent caches), so it is enough that a workgroup's writes have
+// completed -- s_waitcnt 0 waits until the memory system has acknowledged
+// them -- before the completion counter is bumped, and that the last
+// workgroup reads only after it has seen the counter.
+__device__ inline void wait_writes_done() { __builtin_amdgcn_s_waitcnt(0); }
+
 // V bytes of one column for one lane, added into V INT32 accumulators.
 // NT loads carry the nontemporal hint (streamed weights are not re-read).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -311,13 +323,12 @@ __device__ inline void run_unit(const int8_t* __restrict__ W, const float* __res
                 atomicAdd(ws_row + n_tile0 + e, sum);
             }
         }
-        __threadfence();  // release: this unit's adds are visible before it is counted
+        wait_writes_done();  // this unit's atomic adds are performed before it is counted
         __syncthreads();
         if (threadIdx.x == 0)
             s.is_last = atomicAdd(counters_row + tile, 1u) == (uint32_t)(n_slices - 1);
         __syncthreads();
         if (s.is_last) {
-            __threadfence();  // acquire: every other slice's adds are visible
             for (int e = threadIdx.x; e < TB && n_tile0 + e < N; e += S::BLOCK) {
                 const int32_t sum = atomicExch(ws_row + n_tile0 + e, 0);  // read and re-zero
                 store_result<ACC>(out_row, acc_row, scale, n_tile0 + e, sum);

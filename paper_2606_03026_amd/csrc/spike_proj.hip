@@ -128,16 +128,17 @@ const ShapeEntry* default_shape(const void* W, int64_t N, int vec)
     return nullptr;
 }
 
-// Decode-latency shape for one or a few rows: no K-split (the atomic
-// epilogue costs three serialized memory round trips) and narrow tiles so
-// that enough workgroups share the active columns: 64-byte tiles for short
-// rows, 32-byte tiles with 1024-thread workgroups for long ones.
+// Decode-latency plan for one or a few rows (measured on the 1536-wide
+// stack): 64-byte tiles so that enough workgroups share the active columns;
+// short rows (<= 32 mask words) in 256-thread workgroups without a K-split,
+// long rows in 1024-thread workgroups with K-slices of 24 words.
 const ShapeEntry* latency_shape(const void* W, int64_t N, int wpr)
 {
-    const int code = wpr <= 32 ? SPIKE_SHAPE(4, 16, 8, 256) : SPIKE_SHAPE(4, 8, 8, 1024);
+    const int code = wpr <= 32 ? SPIKE_SHAPE(4, 16, 8, 256) : SPIKE_SHAPE(4, 16, 4, 1024);
     const ShapeEntry* e = find_shape(code);
     return shape_fits(e, W, N) ? e : nullptr;
 }
+constexpr int kLatencySliceWords = 24;
 
 constexpr int kMinTile = 32;  // smallest tile of any shape: sizes the counter array
 
@@ -152,13 +153,17 @@ struct spike_proj {
     int32_t* ws = nullptr;         // [max_B][N] INT32, zero between calls
     uint32_t* counters = nullptr;  // [max_B][counter_stride], zero between calls
     int32_t counter_stride = 0;
+    int32_t* parts = nullptr;      // partial tiles of the matrix-core K-split
+    int64_t parts_capacity = 0;    // INT32 entries: kMfmaMaxSplits * min(max_B, 64) * N
     int path = SPIKE_PATH_AUTO;
     int slice_words = 0;  // 0 = automatic
     int max_slices = 16;
     const ShapeEntry* shape = nullptr;  // throughput shape (B above the latency range)
     bool shape_pinned = false;          // set by SPIKE_TUNE_SHAPE / _VEC: used for every B
     int tiles_per_unit = 1;
-    int mfma_min_b = 64;
+    int mfma_min_b = 5;  // measured crossover: the matrix cores win from 8 rows, tie at 4
+    int mfma_waves = 0;        // 0 = automatic
+    int mfma_split_words = 0;  // 0 = automatic
 };
 
 struct spike_stream {
@@ -203,30 +208,41 @@ int alloc_workspace(spike_proj* h, int32_t max_B)
     const size_t ws_bytes = (size_t)max_B * h->N * sizeof(int32_t);
     const int32_t stride = (int32_t)((h->N + kMinTile - 1) / kMinTile);
     const size_t ctr_bytes = (size_t)max_B * stride * sizeof(uint32_t);
+    const int64_t parts_cap = (int64_t)spk::kMfmaMaxSplits * std::min(max_B, spk::kMfmaSplitRows) * h->N;
     int32_t* ws = nullptr;
     uint32_t* ctr = nullptr;
+    int32_t* parts = nullptr;
     hipError_t e = hipMalloc(&ws, ws_bytes);
     if (e != hipSuccess)
         return fail(SPIKE_ENOMEM, "workspace allocation of %zu bytes failed: %s", ws_bytes, hipGetErrorString(e));
     e = hipMalloc(&ctr, ctr_bytes);
+    if (e == hipSuccess)
+        e = hipMalloc(&parts, (size_t)parts_cap * sizeof(int32_t));
     if (e != hipSuccess) {
         (void)hipFree(ws);
-        return fail(SPIKE_ENOMEM, "counter allocation of %zu bytes failed: %s", ctr_bytes, hipGetErrorString(e));
+        if (ctr)
+            (void)hipFree(ctr);
+        return fail(SPIKE_ENOMEM, "workspace allocation failed: %s", hipGetErrorString(e));
     }
     // Zeroed once here; the kernels leave both zeroed after every call.
     if ((e = hipMemset(ws, 0, ws_bytes)) != hipSuccess || (e = hipMemset(ctr, 0, ctr_bytes)) != hipSuccess ||
         (e = hipDeviceSynchronize()) != hipSuccess) {
         (void)hipFree(ws);
         (void)hipFree(ctr);
+        (void)hipFree(parts);
         return hip_fail(e, "workspace initialisation");
     }
     if (h->ws)
         (void)hipFree(h->ws);
     if (h->counters)
         (void)hipFree(h->counters);
+    if (h->parts)
+        (void)hipFree(h->parts);
     h->ws = ws;
     h->counters = ctr;
     h->counter_stride = stride;
+    h->parts = parts;
+    h->parts_capacity = parts_cap;
     h->max_B = max_B;
     return SPIKE_OK;
 }
@@ -287,7 +303,9 @@ GatherPlan plan_gather(const spike_proj* h, int32_t B)
     if (h->slice_words > 0)
         p.sw = std::min(h->slice_words, std::min(h->wpr, spk::kMaxSliceWords));
     else if (latency)
-        p.sw = h->wpr;
+        p.sw = h->wpr <= 32 ? h->wpr : kLatencySliceWords;
+    else if (h->wpr <= spk::kMaxSliceWords)
+        p.sw = h->wpr;  // enough rows x tiles to fill the chip without a K-split
     else
         p.sw = choose_slice_words(h, B, n_groups);
     p.n_slices = (int)((h->wpr + p.sw - 1) / p.sw);
@@ -334,8 +352,14 @@ int forward_impl(spike_proj* h, const uint64_t* mask, int32_t B, float* out, int
         if (!spk::mfma_supported(h->K, h->N, h->W))
             return fail(SPIKE_EUNSUPPORTED, "matrix-core path needs N %% %d == 0 and a %d-byte aligned W",
                         spk::kMfmaNAlign, spk::kMfmaNAlign);
-        const hipError_t e = spk::launch_mfma(h->W, h->scale, h->K, h->N, mask, B, h->slice_words, h->ws,
-                                              h->counters, out, acc, ACC, st);
+        int wps = 0;
+        const int n_splits = spk::mfma_splits(h->K, h->N, B, h->mfma_split_words, &wps);
+        if (n_splits > 1 && (B > spk::kMfmaSplitRows || (int64_t)n_splits * B * h->N > h->parts_capacity))
+            return fail(SPIKE_EUNSUPPORTED, "matrix-core K-split of %d needs B <= %d and %lld partial entries "
+                        "(have %lld)", n_splits, spk::kMfmaSplitRows, (long long)n_splits * B * h->N,
+                        (long long)h->parts_capacity);
+        const hipError_t e = spk::launch_mfma(h->W, h->scale, h->K, h->N, mask, B, wps, n_splits, h->mfma_waves,
+                                              h->parts, h->counters, out, acc, ACC, st);
         return e == hipSuccess ? SPIKE_OK : hip_fail(e, "matrix-core launch");
     }
     return launch_gather<ACC>(h, mask, B, out, acc, st);
@@ -431,6 +455,8 @@ int spike_proj_destroy(spike_proj_t h)
         (void)hipFree(h->ws);
     if (h->counters)
         (void)hipFree(h->counters);
+    if (h->parts)
+        (void)hipFree(h->parts);
     delete h;
     return rc;
 }
@@ -480,6 +506,16 @@ int spike_proj_tune(spike_proj_t h, int32_t key, int32_t value)
         if (value < 1 || value > 4096)
             return fail(SPIKE_EINVAL, "tiles per unit %d outside [1, 4096]", value);
         h->tiles_per_unit = value;
+        return SPIKE_OK;
+    case SPIKE_TUNE_MFMA_SPLIT_WORDS:
+        if (value < 0)
+            return fail(SPIKE_EINVAL, "matrix-core split words must be >= 0, got %d", value);
+        h->mfma_split_words = value;
+        return SPIKE_OK;
+    case SPIKE_TUNE_MFMA_WAVES:
+        if (value != 0 && value != 4 && value != 8)
+            return fail(SPIKE_EINVAL, "matrix-core waves per workgroup must be 0, 4 or 8, got %d", value);
+        h->mfma_waves = value;
         return SPIKE_OK;
     default:
         return fail(SPIKE_EINVAL, "unknown tuning key %d", key);

@@ -69,6 +69,7 @@ SHAPES = [(0, 0), (1, 1), (0, 1), (4, 3)]
 
 
 def apply_shape(sp, h, vec, sw):
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_GATHER)
     if vec:
         try:
             sp.spike_proj_tune(h, sp.SPIKE_TUNE_VEC, vec)
@@ -102,6 +103,7 @@ def test_small_shapes(sp, K, N):
 def test_every_vector_width_on_the_decode_shape(sp, vec):
     d = wl.single_projection(n_masks=6)
     h, *_ = make(sp, d["W"], d["scale"])
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_GATHER)
     sp.spike_proj_tune(h, sp.SPIKE_TUNE_VEC, vec)
     for sw in (0, 1, 5, 24):
         sp.spike_proj_tune(h, sp.SPIKE_TUNE_SLICE_WORDS, sw)
@@ -325,6 +327,7 @@ def test_workspace_resets_between_calls(sp):
     or counter left dirty by one call would corrupt the next."""
     d = wl.down_sweep(0.1, n_masks=40)
     h, *_ = make(sp, d["W"], d["scale"])
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_GATHER)
     sp.spike_proj_tune(h, sp.SPIKE_TUNE_SLICE_WORDS, 1)
     ref = oracle.spike_forward(d["W"], d["scale"], d["masks"])
     outs, lo = [], 0
@@ -438,6 +441,7 @@ def test_every_instantiated_shape(sp, K, N):
     and with several tiles per workgroup, gives the oracle's bits."""
     p = wl.small_problem(K, N, 3, 0.2, seed=K ^ N)
     h, *_ = make(sp, p["W"], p["scale"])
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_GATHER)
     wpr = wl.words_per_row(K)
     ran = 0
     for code in sp.spike_proj_shapes():
@@ -490,9 +494,13 @@ def test_matrix_core_path(sp, B, K, N):
     h, *_ = make(sp, p["W"], p["scale"])
     sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
     wpr = wl.words_per_row(K)
-    for wps in (0, 1, 3, wpr):
-        sp.spike_proj_tune(h, sp.SPIKE_TUNE_SLICE_WORDS, min(wps, 256))
-        assert_parity(sp, h, p["W"], p["scale"], p["masks"])
+    # K-splits across workgroups exist for one row tile (B <= 64), at most 8
+    splits = (0, -(-wpr // 8), -(-wpr // 3), wpr) if B <= 64 else (0, wpr)
+    for wps in splits:
+        for waves in (0, 4, 8):
+            sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_SPLIT_WORDS, wps)
+            sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_WAVES, waves)
+            assert_parity(sp, h, p["W"], p["scale"], p["masks"])
 
 
 def test_matrix_core_extremes(sp):
@@ -531,3 +539,30 @@ def test_paths_agree_on_prefill_and_padding_junk(sp):
         sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, path)
         outs[path] = bits32(gpu_forward(sp, h, masks))
     np.testing.assert_array_equal(outs[sp.SPIKE_PATH_GATHER], outs[sp.SPIKE_PATH_MFMA])
+
+
+@pytest.mark.parametrize("waves", [4, 8])
+def test_matrix_core_waves_per_workgroup(sp, waves):
+    p = wl.small_problem(6144, 1536, 60, 0.12, seed=waves)
+    h, *_ = make(sp, p["W"], p["scale"])
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_WAVES, waves)
+    for wps in (0, 12, 13, 40, 96):
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_SPLIT_WORDS, wps)
+        assert_parity(sp, h, p["W"], p["scale"], p["masks"])
+
+
+def test_matrix_core_split_limits(sp):
+    """A K-split is refused (not run) when it needs more partial tiles than
+    the handle holds or more than one row tile."""
+    p = wl.small_problem(6144, 128, 100, 0.1, seed=3)
+    h, *_ = make(sp, p["W"], p["scale"])
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
+    out = torch.empty((100, 128), device="cuda")
+    for B, wps in ((100, 12), (10, 1)):  # two row tiles / 96 splits
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_SPLIT_WORDS, wps)
+        with pytest.raises(sp.SpikeError) as e:
+            sp.spike_proj_forward(h, dmask(p["masks"][:B]), B, out)
+        assert e.value.code == sp.SPIKE_EUNSUPPORTED
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_SPLIT_WORDS, 0)
+    assert_parity(sp, h, p["W"], p["scale"], p["masks"])
