@@ -159,7 +159,7 @@ int spike_stack_forward(const spike_proj_t *projs, int32_t n_proj, const uint64_
  * tokens, each running n_proj projections, all in one launch.  projs holds
  * n_sets * n_proj handles; token t uses projs[(t % n_sets) * n_proj + j]
  * (n_sets > 1 rotates address-distinct weight copies).  All handles must
- * share N.  Per token, masks hold the projections' rows back to back
+ * share N; 1 <= n_proj <= 64 and every K <= 16384.  Per token, masks hold the projections' rows back to back
  * (token stride sum_j ceil(K_j/64) words) and out holds n_proj * N floats.
  * create() copies a small descriptor table to the device (allocates);
  * forward() only launches. */

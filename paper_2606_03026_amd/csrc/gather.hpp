@@ -275,17 +275,52 @@ constexpr size_t unit_dyn_lds(int slice_words, int tiles_per_unit)
     return tiles_per_unit == 1 ? (l > r ? l : r) : l + r;
 }
 
+// Descriptor of one projection in a multi-projection stream.
+struct StreamDesc {
+    const int8_t* W;
+    const float* scale;
+    int32_t K;
+    int32_t wpr;
+    int64_t mask_off;  // word offset of this projection's row within a token
+    int64_t out_off;   // float offset of this projection's output within a token
+};
+
+// Per-projection layout of a token, passed by value as a kernel argument so
+// that a workgroup can start loading its spike words before the descriptor
+// (weight and scale pointers) has arrived from memory.
+constexpr int kStreamMaxProj = 64;
+struct StreamLayout {
+    int32_t K[kStreamMaxProj];
+    int32_t mask_off[kStreamMaxProj];  // word offset of the projection's row within a token
+};
+
+// Many independent batch-1 projections in one launch: unit id -> (token,
+// projection, tile group); each unit walks the whole K axis of its row, so
+// no cross-unit reduction is needed.
+// Weight and scale pointers of a unit, given directly or read from a
+// stream descriptor once the spike words have been requested.
+struct DirectOperands {
+    const int8_t* W;
+    const float* scale;
+    __device__ const int8_t* weights() const { return W; }
+    __device__ const float* scales() const { return scale; }
+};
+__device__ inline DirectOperands operands_of(const DirectOperands& d) { return d; }
+__device__ inline DirectOperands operands_of(const StreamDesc* d) { return DirectOperands{d->W, d->scale}; }
+
 // One unit: K-slice [w0, w0 + nw) of one row, tiles [tile0, tile0 + n_tiles_here).
-template <class S, bool ACC>
-__device__ inline void run_unit(const int8_t* __restrict__ W, const float* __restrict__ scale, int K, int N,
-                                const uint64_t* __restrict__ row, int w0, int nw, int tile0, int n_tiles_here,
-                                int n_slices, int32_t* ws_row, uint32_t* counters_row, float* out_row,
-                                int32_t* acc_row, SliceLds<S::BLOCK>& s, uint8_t* dyn)
+template <class S, bool ACC, class Src>
+__device__ inline void run_unit(const Src& src, int K, int N, const uint64_t* __restrict__ row, int w0, int nw,
+                                int tile0, int n_tiles_here, int n_slices, int32_t* ws_row, uint32_t* counters_row,
+                                float* out_row, int32_t* acc_row, SliceLds<S::BLOCK>& s, uint8_t* dyn)
 {
     constexpr int TB = S::kTile;
     constexpr int G = S::kGroups;
     uint16_t* list = reinterpret_cast<uint16_t*>(dyn);
     const int cnt = compact_slice<S::BLOCK>(row, w0, nw, K, s, [&](int pos, int k) { list[pos] = (uint16_t)k; });
+    const DirectOperands ops = operands_of(src);
+    const int8_t* __restrict__ W = ops.weights();
+    const float* __restrict__ scale = ops.scales();
     int32_t* red = reinterpret_cast<int32_t*>(n_tiles_here == 1 ? dyn : dyn + list_lds<S>(nw));
 
     const int lg = threadIdx.x % S::LG;
@@ -362,30 +397,17 @@ __global__ __launch_bounds__(S::BLOCK) __attribute__((amdgpu_waves_per_eu(4))) v
     const int tile0 = tg * tiles_per_unit;
     const int nt = min(tiles_per_unit, n_tiles - tile0);
     const int64_t rowN = (int64_t)b * N;
-    run_unit<S, ACC>(W, scale, K, N, mask + (int64_t)b * wpr, w0, nw, tile0, nt, n_slices,
+    run_unit<S, ACC>(DirectOperands{W, scale}, K, N, mask + (int64_t)b * wpr, w0, nw, tile0, nt, n_slices,
                      n_slices > 1 ? ws + rowN : nullptr,
                      n_slices > 1 ? counters + (int64_t)b * counter_stride : nullptr, ACC ? nullptr : out + rowN,
                      ACC ? acc_out + rowN : nullptr, s, dyn);
 }
 
-// Descriptor of one projection in a multi-projection stream.
-struct StreamDesc {
-    const int8_t* W;
-    const float* scale;
-    int32_t K;
-    int32_t wpr;
-    int64_t mask_off;  // word offset of this projection's row within a token
-    int64_t out_off;   // float offset of this projection's output within a token
-};
-
-// Many independent batch-1 projections in one launch: unit id -> (token,
-// projection, tile group); each unit walks the whole K axis of its row, so
-// no cross-unit reduction is needed.
 template <class S>
-__global__ __launch_bounds__(S::BLOCK) __attribute__((amdgpu_waves_per_eu(4))) void k_stream(const StreamDesc* __restrict__ desc, int n_proj, int n_sets,
-                                                     int N, int n_tiles, int tiles_per_unit, int n_items,
-                                                     int xcd_spread, const uint64_t* __restrict__ masks,
-                                                     int64_t mask_stride, float* out, int64_t out_stride)
+__global__ __launch_bounds__(S::BLOCK) __attribute__((amdgpu_waves_per_eu(4))) void k_stream(
+    const StreamDesc* __restrict__ desc, const StreamLayout layout, int n_proj, int n_sets, int N, int n_tiles,
+    int tiles_per_unit, int n_items, int xcd_spread, const uint64_t* __restrict__ masks, int64_t mask_stride,
+    float* out, int64_t out_stride)
 {
     __shared__ SliceLds<S::BLOCK> s;
     extern __shared__ __align__(16) uint8_t dyn[];
@@ -406,11 +428,13 @@ __global__ __launch_bounds__(S::BLOCK) __attribute__((amdgpu_waves_per_eu(4))) v
     }
     const int t = item / n_proj;
     const int j = item - t * n_proj;
-    const StreamDesc d = desc[(t % n_sets) * n_proj + j];
+    const int K = layout.K[j];
+    const uint64_t* row = masks + (int64_t)t * mask_stride + layout.mask_off[j];
+    const StreamDesc* d = desc + (t % n_sets) * n_proj + j;  // read after the spike words are requested
     const int tile0 = tg * tiles_per_unit;
     const int nt = min(tiles_per_unit, n_tiles - tile0);
-    run_unit<S, false>(d.W, d.scale, d.K, N, masks + (int64_t)t * mask_stride + d.mask_off, 0, d.wpr, tile0, nt, 1,
-                       nullptr, nullptr, out + (int64_t)t * out_stride + d.out_off, nullptr, s, dyn);
+    run_unit<S, false>(d, K, N, row, 0, (K + 63) / 64, tile0, nt, 1, nullptr, nullptr,
+                       out + (int64_t)t * out_stride + (int64_t)j * N, nullptr, s, dyn);
 }
 
 // Standalone active-index extraction: one workgroup per row, chunks of

@@ -175,6 +175,7 @@ struct spike_stream {
     int device = 0;
     int64_t mask_stride = 0, out_stride = 0;
     spk::StreamDesc* d_desc = nullptr;
+    spk::StreamLayout layout{};
     std::vector<const void*> weights;  // to re-check alignment when the shape changes
 };
 
@@ -198,9 +199,9 @@ void launch_stream_t(const spike_stream* s, int n_tiles, unsigned units, const u
 {
     const size_t dyn = spk::unit_dyn_lds<S>(s->max_wpr, s->tiles_per_unit);
     const int n_items = s->n_tokens * s->n_proj;
-    hipLaunchKernelGGL((spk::k_stream<S>), dim3(units), dim3(S::BLOCK), dyn, st, s->d_desc, s->n_proj, s->n_sets,
-                       s->N, n_tiles, s->tiles_per_unit, n_items, s->xcd_spread, masks, s->mask_stride, out,
-                       s->out_stride);
+    hipLaunchKernelGGL((spk::k_stream<S>), dim3(units), dim3(S::BLOCK), dyn, st, s->d_desc, s->layout, s->n_proj,
+                       s->n_sets, s->N, n_tiles, s->tiles_per_unit, n_items, s->xcd_spread, masks, s->mask_stride,
+                       out, s->out_stride);
 }
 
 int alloc_workspace(spike_proj* h, int32_t max_B)
@@ -575,6 +576,8 @@ int spike_stream_create(const spike_proj_t* projs, int32_t n_proj, int32_t n_set
     *out_stream = nullptr;
     if (!projs || n_proj < 1 || n_sets < 1 || n_tokens < 1)
         return fail(SPIKE_EINVAL, "n_proj, n_sets and n_tokens must be >= 1");
+    if (n_proj > spk::kStreamMaxProj)
+        return fail(SPIKE_EUNSUPPORTED, "a stream holds at most %d projections per token", spk::kStreamMaxProj);
     const int64_t n_handles = (int64_t)n_proj * n_sets;
     if (!projs[0])
         return fail(SPIKE_EINVAL, "projection 0 is null");
@@ -640,6 +643,14 @@ int spike_stream_create(const spike_proj_t* projs, int32_t n_proj, int32_t n_set
     s->max_wpr = max_wpr;
     s->mask_stride = moff;
     s->out_stride = (int64_t)n_proj * N;
+    for (int j = 0; j < n_proj; ++j) {
+        s->layout.K[j] = desc[j].K;
+        s->layout.mask_off[j] = (int32_t)desc[j].mask_off;
+    }
+    if (moff > 0x7fffffff) {
+        delete s;
+        return fail(SPIKE_EUNSUPPORTED, "token mask stride too large");
+    }
     s->weights = std::move(weights);
     hipError_t e = hipGetDevice(&s->device);
     if (e == hipSuccess)
