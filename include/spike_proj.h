@@ -111,6 +111,8 @@ int spike_proj_destroy(spike_proj_t h);
  *                           tiles of one (token, projection) on one XCD
  *   SPIKE_TUNE_MFMA_WAVES   waves per workgroup of the matrix-core path, which
  *                           share one tile's K range: 0 = automatic, 4, 8
+ *   SPIKE_TUNE_MFMA_DEPTH   k-steps of weights in flight per wave of the
+ *                           matrix-core path: 0 = automatic, 1, 2, 4
  *   SPIKE_TUNE_MFMA_SPLIT_WORDS  mask words per K-split of the matrix-core
  *                           path (0 = automatic).  Splits exist only for
  *                           B <= 64 and at most 8 of them; a forward that
@@ -127,6 +129,7 @@ int spike_proj_destroy(spike_proj_t h);
 #define SPIKE_TUNE_XCD_SPREAD 8
 #define SPIKE_TUNE_MFMA_WAVES 9
 #define SPIKE_TUNE_MFMA_SPLIT_WORDS 10
+#define SPIKE_TUNE_MFMA_DEPTH 11
 #define SPIKE_SHAPE(V, LG, U, BLOCK) ((V) | ((LG) << 5) | ((U) << 15) | (((BLOCK) / 64) << 20))
 #define SPIKE_SHAPE_NT (1 << 25) /* or-ed into a shape code: nontemporal weight loads */
 #define SPIKE_PATH_AUTO 0

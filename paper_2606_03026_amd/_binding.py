@@ -17,7 +17,7 @@ from .build import LIB
 SPIKE_OK, SPIKE_EINVAL, SPIKE_EHIP, SPIKE_ENOMEM, SPIKE_EUNSUPPORTED = 0, -1, -2, -3, -4
 SPIKE_TUNE_PATH, SPIKE_TUNE_SLICE_WORDS, SPIKE_TUNE_MFMA_MIN_B, SPIKE_TUNE_VEC, SPIKE_TUNE_MAX_SLICES = 1, 2, 3, 4, 5
 SPIKE_TUNE_SHAPE, SPIKE_TUNE_TILES_PER_UNIT, SPIKE_TUNE_XCD_SPREAD, SPIKE_TUNE_MFMA_WAVES = 6, 7, 8, 9
-SPIKE_TUNE_MFMA_SPLIT_WORDS = 10
+SPIKE_TUNE_MFMA_SPLIT_WORDS, SPIKE_TUNE_MFMA_DEPTH = 10, 11
 SPIKE_SHAPE_NT = 1 << 25
 SPIKE_PATH_AUTO, SPIKE_PATH_GATHER, SPIKE_PATH_MFMA = 0, 1, 2
 SPIKE_DEFAULT_MAX_B = 512

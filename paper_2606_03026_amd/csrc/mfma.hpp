@@ -38,14 +38,18 @@ constexpr int kMfmaNAlign = 64;  // N must be a multiple of this; W 4-byte align
 constexpr int kMfmaRows = 64;    // spike rows per tile (4 subtiles of 16)
 constexpr int kMfmaCols = 64;    // channels per tile (4 MFMA channel sets of 16)
 constexpr int kMfmaK = 64;       // k per step: one mask word
-constexpr int kXPitch = 80;      // LDS bytes per expanded row (64 + 16 padding)
+constexpr int kXRow = 64;        // LDS bytes per expanded spike row (quarters swizzled)
+constexpr int kMfmaDefaultDepth = 2;  // k-steps of weights in flight per wave
 
 typedef int32_t mf_i32x4 __attribute__((ext_vector_type(4)));
 
+constexpr int kBufferWordFormat = 0x00020000;  // buffer resource word 3: 32-bit data format (gfx9)
+
+// The weight matrix must be addressable by 32-bit byte offsets (one buffer
+// resource): K * N < 2^31.
 inline bool mfma_supported(int K, int N, const void* W)
 {
-    (void)K;
-    return N % kMfmaNAlign == 0 && reinterpret_cast<uintptr_t>(W) % 4 == 0;
+    return N % kMfmaNAlign == 0 && reinterpret_cast<uintptr_t>(W) % 4 == 0 && (int64_t)K * N < (1ll << 31);
 }
 
 // Four spike bits -> four bytes holding 0 or 1 (bit i -> byte i).
@@ -66,7 +70,7 @@ __device__ inline void transpose4x4(uint32_t d0, uint32_t d1, uint32_t d2, uint3
     e3 = __builtin_amdgcn_perm(hi23, hi01, 0x07060302u);
 }
 
-template <int KW, bool ACC>
+template <int KW, int D, int NS, bool ACC>
 __global__ __launch_bounds__(64 * KW) void k_mfma(const int8_t* __restrict__ W, const float* __restrict__ scale,
                                                   int K, int N, const uint64_t* __restrict__ mask, int wpr, int B,
                                                   int words_per_split, int n_splits, int n_coltiles,
@@ -75,11 +79,13 @@ __global__ __launch_bounds__(64 * KW) void k_mfma(const int8_t* __restrict__ W, 
 {
     constexpr int BLOCK = 64 * KW;
     constexpr int TILE = kMfmaRows * kMfmaCols;
-    __shared__ __align__(16) uint8_t xs[KW][kMfmaRows * kXPitch];  // one area per wave
+    __shared__ __align__(16) uint8_t xs[KW][kMfmaRows * kXRow];  // one area per wave
     __shared__ int32_t red[TILE];                                  // the tile's INT32 sums
     __shared__ int32_t is_last;
 
-    const int wave = threadIdx.x / 64;
+    // wave index as a scalar, so that everything derived from it (k-steps,
+    // buffer offsets) is known to be uniform across the wave
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
     const int l = threadIdx.x % 64;
     const int q = l / 16;  // k-group of the operands, row group of the result
     const int c = l % 16;  // row of A, column of B and of the result
@@ -94,31 +100,40 @@ __global__ __launch_bounds__(64 * KW) void k_mfma(const int8_t* __restrict__ W, 
 
     for (int e = threadIdx.x; e < TILE; e += BLOCK)
         red[e] = 0;
+    __syncthreads();
 
     uint8_t* xw = xs[wave];
-    const int8_t* wbase = W + n0 + 4 * c;
     const int xb = m0 + l;  // the row this lane stages
-    // W: 4 channels (n0 + 4c ..) of k-rows kb + 16q + i, i < 16 (rows past K
-    // are clamped to a valid row; their spikes are zero).
+    // W: 4 channels (n0 + 4c ..) of k-rows kb + 16q + i, i < 16.  For a full
+    // step the row base of each i is the same in every lane (a scalar
+    // register) and the lane adds a 32-bit offset, so the addresses cost no
+    // vector ALU; in the last, partial step rows past K are clamped to a
+    // valid row (their spikes are zero).
+    // Buffer loads: the weight matrix is one buffer resource (scalar
+    // registers), the lane adds a fixed 32-bit offset and each of the 16
+    // rows a scalar offset, so the addresses cost no vector ALU.  Offsets at
+    // or past K*N (rows beyond K in the last step) read 0 instead of memory.
+    const __amdgpu_buffer_rsrc_t wrsrc =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(W), 0, K * N, kBufferWordFormat);
+    const int lane_off = 16 * q * N + 4 * c;
     auto load_w = [&](int w, uint32_t (&d)[16]) {
-        const int kb = w * kMfmaK;
+        const int row0 = w * kMfmaK * N + n0;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int k = min(kb + 16 * q + i, K - 1);
-            d[i] = *reinterpret_cast<const uint32_t*>(wbase + (int64_t)k * N);
-        }
+        for (int i = 0; i < 16; ++i)
+            d[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(wrsrc, lane_off, row0 + i * N, 0);
     };
-    auto load_bits = [&](int w) -> uint64_t {
-        if (xb >= B)
-            return 0;
-        uint64_t word = mask[(int64_t)xb * wpr + w];
+    // The raw word is kept in flight; bits at or above K are cleared only
+    // when it is staged, so that issuing the load never waits for it.
+    auto load_bits = [&](int w) -> uint64_t { return xb < B ? mask[(int64_t)xb * wpr + w] : 0ull; };
+    // this lane's row of the wave's LDS area <- the 64 spikes of step w as
+    // 0/1 bytes.  Rows are 64 bytes; the four 16-byte quarters of row r sit
+    // at quarter slot q ^ ((r >> 1) & 3), which makes both the row writes
+    // here and the operand reads below free of LDS bank conflicts (any 8
+    // consecutive lanes touch all 32 banks once).
+    auto stage = [&](uint64_t word, int w) {
         const int valid = K - 64 * w;
         if (valid < 64)
             word &= valid <= 0 ? 0ull : ((1ull << valid) - 1ull);
-        return word;
-    };
-    // this lane's row of the wave's LDS area <- 64 spikes as 0/1 bytes
-    auto stage = [&](uint64_t word) {
 #pragma unroll
         for (int qq = 0; qq < 4; ++qq) {
             const uint32_t bits = (uint32_t)(word >> (16 * qq));
@@ -127,7 +142,7 @@ __global__ __launch_bounds__(64 * KW) void k_mfma(const int8_t* __restrict__ W, 
             v.y = expand_nibble(bits >> 4);
             v.z = expand_nibble(bits >> 8);
             v.w = expand_nibble(bits >> 12);
-            *reinterpret_cast<uint4*>(&xw[l * kXPitch + qq * 16]) = v;
+            *reinterpret_cast<uint4*>(&xw[l * kXRow + ((qq ^ ((l >> 1) & 3)) * 16)]) = v;
         }
     };
 
@@ -138,55 +153,86 @@ __global__ __launch_bounds__(64 * KW) void k_mfma(const int8_t* __restrict__ W, 
         for (int t = 0; t < 4; ++t)
             acc[ms][t] = mf_i32x4{0, 0, 0, 0};
 
-    // Each wave walks k-steps wave, wave + KW, ... of the range on its own:
-    // its LDS area is private, so only wave-level ordering is needed (LDS
-    // operations of one wave complete in order).
-    uint32_t wc[16], wn[16];
-    int w = w_begin + wave;
-    if (w < w_end) {
-        load_w(w, wc);
-        stage(load_bits(w));
-    }
-    for (; w < w_end; w += KW) {
-        const bool more = w + KW < w_end;
-        uint64_t nbits = 0;
-        if (more) {
-            load_w(w + KW, wn);
-            nbits = load_bits(w + KW);
-        }
+    // Each wave walks k-steps wave, wave + KW, ... of the range on its own,
+    // with the weights and spike words of the next D steps in flight (a ring
+    // of D register slots; the loop is unrolled by D so slot indices stay
+    // static).  The wave's LDS area is private, so only wave-level ordering
+    // is needed (LDS operations of one wave complete in order).
+    const int n_steps = w_begin + wave < w_end ? (w_end - w_begin - wave + KW - 1) / KW : 0;
+    // Loads are issued unconditionally, for a step index clamped to the
+    // wave's last step (extra loads re-read cached data): a conditional
+    // refill would turn the ring slots into phis that the compiler fills
+    // with copies, and every copy waits for its load.
+    const int last_w = w_begin + wave + (n_steps - 1) * KW;
+    auto step_w = [&](int i) { return min(w_begin + wave + i * KW, last_w); };
+    uint32_t wbuf[D][16];
+    uint64_t bits[D];
+    // one k-step: consume ring slot d (step i), refill it with step i + D
+    auto step = [&](int d, int i, bool live) {
+        stage(live ? bits[d] : 0ull, step_w(i));
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         mf_i32x4 a[4];
 #pragma unroll
-        for (int ms = 0; ms < 4; ++ms)
-            a[ms] = *reinterpret_cast<const mf_i32x4*>(&xw[(ms * 16 + c) * kXPitch + q * 16]);
+        for (int ms = 0; ms < 4; ++ms) {
+            const int r = ms * 16 + c;
+            a[ms] = *reinterpret_cast<const mf_i32x4*>(&xw[r * kXRow + ((q ^ ((r >> 1) & 3)) * 16)]);
+        }
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         mf_i32x4 f[4];
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
             uint32_t e0, e1, e2, e3;
-            transpose4x4(wc[4 * m], wc[4 * m + 1], wc[4 * m + 2], wc[4 * m + 3], e0, e1, e2, e3);
+            transpose4x4(wbuf[d][4 * m], wbuf[d][4 * m + 1], wbuf[d][4 * m + 2], wbuf[d][4 * m + 3], e0, e1, e2, e3);
             f[0][m] = (int32_t)e0;
             f[1][m] = (int32_t)e1;
             f[2][m] = (int32_t)e2;
             f[3][m] = (int32_t)e3;
         }
-        if (more)
-            stage(nbits);  // the A-operands of this step are already in registers
+        // Keep the refill below the transposes that read the old slot: if the
+        // scheduler hoists it, old and new values live in different
+        // registers and the ring turns into copies that wait for the loads.
+        __builtin_amdgcn_sched_barrier(0);
+        load_w(step_w(i + D), wbuf[d]);
+        bits[d] = load_bits(step_w(i + D));
+        if (live) {
 #pragma unroll
-        for (int ms = 0; ms < 4; ++ms)
+            for (int ms = 0; ms < 4; ++ms)
 #pragma unroll
-            for (int t = 0; t < 4; ++t)
-                acc[ms][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ms], f[t], acc[ms][t], 0, 0, 0);
-        if (more) {
+                for (int t = 0; t < 4; ++t)
+                    acc[ms][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[ms], f[t], acc[ms][t], 0, 0, 0);
+        }
+    };
+    if (n_steps > 0) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i)
-                wc[i] = wn[i];
+        for (int d = 0; d < D; ++d) {
+            load_w(step_w(d), wbuf[d]);
+            bits[d] = load_bits(step_w(d));
+        }
+        if (NS > 0 && n_steps == NS) {
+            // The common step counts are unrolled completely: with no loop
+            // back-edge there are no phis for the compiler to fill with
+            // copies of the ring that wait for their loads.
+#pragma unroll
+            for (int i = 0; i < NS; ++i)
+                step(i % D, i, true);
+        } else {
+            const int n_full = n_steps / D * D;
+            int i0 = 0;
+            for (; i0 < n_full; i0 += D) {
+#pragma unroll
+                for (int d = 0; d < D; ++d)
+                    step(d, i0 + d, true);
+            }
+#pragma unroll
+            for (int d = 0; d < D; ++d)
+                if (i0 + d < n_steps)
+                    step(d, i0 + d, true);
         }
     }
 
-    __syncthreads();  // red is zeroed everywhere
+    __syncthreads();  // every wave is done with its steps
 #pragma unroll
     for (int ms = 0; ms < 4; ++ms)
 #pragma unroll
@@ -273,7 +319,7 @@ inline int mfma_splits(int K, int N, int B, int words_per_split_req, int* wps_ou
     return (wpr + wps - 1) / wps;
 }
 
-template <int KW>
+template <int KW, int D, int NS>
 hipError_t launch_mfma_t(const int8_t* W, const float* scale, int K, int N, const uint64_t* mask, int B, int wps,
                          int n_splits, int32_t* parts, uint32_t* counters, float* out, int32_t* acc, bool want_acc,
                          hipStream_t st)
@@ -285,26 +331,55 @@ hipError_t launch_mfma_t(const int8_t* W, const float* scale, int K, int N, cons
     if (units > 0x7fffffff)
         return hipErrorInvalidValue;
     if (want_acc)
-        hipLaunchKernelGGL((k_mfma<KW, true>), dim3((unsigned)units), dim3(64 * KW), 0, st, W, scale, K, N, mask,
-                           wpr, B, wps, n_splits, n_coltiles, parts, counters, out, acc);
+        hipLaunchKernelGGL((k_mfma<KW, D, NS, true>), dim3((unsigned)units), dim3(64 * KW), 0, st, W, scale, K, N,
+                           mask, wpr, B, wps, n_splits, n_coltiles, parts, counters, out, acc);
     else
-        hipLaunchKernelGGL((k_mfma<KW, false>), dim3((unsigned)units), dim3(64 * KW), 0, st, W, scale, K, N, mask,
-                           wpr, B, wps, n_splits, n_coltiles, parts, counters, out, acc);
+        hipLaunchKernelGGL((k_mfma<KW, D, NS, false>), dim3((unsigned)units), dim3(64 * KW), 0, st, W, scale, K, N,
+                           mask, wpr, B, wps, n_splits, n_coltiles, parts, counters, out, acc);
     return hipGetLastError();
 }
 
 // waves_req: 0 = automatic (8 waves per workgroup share a tile's K range,
-// measured best or equal at every batch size tried).
+// measured best or equal at every batch size tried).  depth_req: k-steps in
+// flight per wave, 0 = automatic.  The step counts per wave that the
+// automatic splits produce (3, 6, 12 for 8 waves) get fully unrolled kernels.
 inline hipError_t launch_mfma(const int8_t* W, const float* scale, int K, int N, const uint64_t* mask, int B,
-                              int wps, int n_splits, int waves_req, int32_t* parts, uint32_t* counters, float* out,
-                              int32_t* acc, bool want_acc, hipStream_t st)
+                              int wps, int n_splits, int waves_req, int depth_req, int32_t* parts,
+                              uint32_t* counters, float* out, int32_t* acc, bool want_acc, hipStream_t st)
 {
     const int waves = waves_req == 0 ? 8 : waves_req;
-    switch (waves) {
-    case 4: return launch_mfma_t<4>(W, scale, K, N, mask, B, wps, n_splits, parts, counters, out, acc, want_acc, st);
-    case 8: return launch_mfma_t<8>(W, scale, K, N, mask, B, wps, n_splits, parts, counters, out, acc, want_acc, st);
-    default: return hipErrorInvalidValue;
+    const int depth = depth_req == 0 ? kMfmaDefaultDepth : depth_req;
+    // steps per wave when every split spans wps words (the last split may be shorter)
+    const int wpr = (K + 63) / 64;
+    const bool uniform = wpr % wps == 0;
+    const int ns = uniform && wps % waves == 0 ? wps / waves : 0;
+#define SPK_MFMA_CASE(KW, D)                                                                                       \
+    if (waves == KW && depth == D) {                                                                               \
+        if (ns == 3)                                                                                               \
+            return launch_mfma_t<KW, D, 3>(W, scale, K, N, mask, B, wps, n_splits, parts, counters, out, acc,      \
+                                           want_acc, st);                                                          \
+        if (ns == 6)                                                                                               \
+            return launch_mfma_t<KW, D, 6>(W, scale, K, N, mask, B, wps, n_splits, parts, counters, out, acc,      \
+                                           want_acc, st);                                                          \
+        if (ns == 12)                                                                                              \
+            return launch_mfma_t<KW, D, 12>(W, scale, K, N, mask, B, wps, n_splits, parts, counters, out, acc,     \
+                                            want_acc, st);                                                         \
+        return launch_mfma_t<KW, D, 0>(W, scale, K, N, mask, B, wps, n_splits, parts, counters, out, acc,          \
+                                       want_acc, st);                                                              \
     }
+    SPK_MFMA_CASE(4, 1)
+    SPK_MFMA_CASE(4, 2)
+    SPK_MFMA_CASE(8, 1)
+    SPK_MFMA_CASE(8, 2)
+#undef SPK_MFMA_CASE
+    // four steps in flight: generic loop only (unrolled, it runs out of registers)
+    if (depth == 4 && waves == 4)
+        return launch_mfma_t<4, 4, 0>(W, scale, K, N, mask, B, wps, n_splits, parts, counters, out, acc, want_acc,
+                                      st);
+    if (depth == 4 && waves == 8)
+        return launch_mfma_t<8, 4, 0>(W, scale, K, N, mask, B, wps, n_splits, parts, counters, out, acc, want_acc,
+                                      st);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace spk

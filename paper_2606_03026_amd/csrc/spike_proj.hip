@@ -164,6 +164,7 @@ struct spike_proj {
     int mfma_min_b = 5;  // measured crossover: the matrix cores win from 8 rows, tie at 4
     int mfma_waves = 0;        // 0 = automatic
     int mfma_split_words = 0;  // 0 = automatic
+    int mfma_depth = 0;        // 0 = automatic
 };
 
 struct spike_stream {
@@ -360,7 +361,7 @@ int forward_impl(spike_proj* h, const uint64_t* mask, int32_t B, float* out, int
                         "(have %lld)", n_splits, spk::kMfmaSplitRows, (long long)n_splits * B * h->N,
                         (long long)h->parts_capacity);
         const hipError_t e = spk::launch_mfma(h->W, h->scale, h->K, h->N, mask, B, wps, n_splits, h->mfma_waves,
-                                              h->parts, h->counters, out, acc, ACC, st);
+                                              h->mfma_depth, h->parts, h->counters, out, acc, ACC, st);
         return e == hipSuccess ? SPIKE_OK : hip_fail(e, "matrix-core launch");
     }
     return launch_gather<ACC>(h, mask, B, out, acc, st);
@@ -512,6 +513,11 @@ int spike_proj_tune(spike_proj_t h, int32_t key, int32_t value)
         if (value < 0)
             return fail(SPIKE_EINVAL, "matrix-core split words must be >= 0, got %d", value);
         h->mfma_split_words = value;
+        return SPIKE_OK;
+    case SPIKE_TUNE_MFMA_DEPTH:
+        if (value != 0 && value != 1 && value != 2 && value != 4)
+            return fail(SPIKE_EINVAL, "matrix-core depth must be 0, 1, 2 or 4, got %d", value);
+        h->mfma_depth = value;
         return SPIKE_OK;
     case SPIKE_TUNE_MFMA_WAVES:
         if (value != 0 && value != 4 && value != 8)

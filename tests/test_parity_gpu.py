@@ -542,12 +542,14 @@ def test_paths_agree_on_prefill_and_padding_junk(sp):
 
 
 @pytest.mark.parametrize("waves", [4, 8])
-def test_matrix_core_waves_per_workgroup(sp, waves):
-    p = wl.small_problem(6144, 1536, 60, 0.12, seed=waves)
+@pytest.mark.parametrize("depth", [1, 2, 4])
+def test_matrix_core_waves_and_depth(sp, waves, depth):
+    p = wl.small_problem(6144 - 64 * 3 + 5, 1536, 60, 0.12, seed=waves * depth)
     h, *_ = make(sp, p["W"], p["scale"])
     sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
     sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_WAVES, waves)
-    for wps in (0, 12, 13, 40, 96):
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_DEPTH, depth)
+    for wps in (0, 12, 13, 40, 94):
         sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_SPLIT_WORDS, wps)
         assert_parity(sp, h, p["W"], p["scale"], p["masks"])
 
