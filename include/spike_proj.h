@@ -28,8 +28,11 @@
  * unchanged until destroy()).  The handle owns a small INT32 workspace of
  * max_B * N entries plus completion counters; the kernels leave it zeroed
  * after every call, so forward() performs no allocation, memset or host
- * synchronisation and can be captured into a HIP graph.  A handle must not
- * run on two streams at the same time (its workspace is shared).
+ * synchronisation and can be captured into a HIP graph.  When N % 64 == 0
+ * the handle also owns a copy of W in the matrix cores' operand order
+ * (ceil(K/64) * 64 * N bytes, made once by create(); the matrix-core path
+ * reads only that copy, so W must not change after create()).  A handle
+ * must not run on two streams at the same time (its workspace is shared).
  *
  * Errors: every entry point returns SPIKE_OK (0) or a negative code;
  * spike_proj_last_error() returns a message for the calling thread's last
@@ -62,8 +65,11 @@ typedef struct spike_stream *spike_stream_t;
  * FP32 scales [N] (Sec. 2.2: binary-input projections are stored
  * column-major; Sec. 2.3: one scale per output channel).  1 <= K <=
  * SPIKE_MAX_K, 1 <= N <= SPIKE_MAX_N.  Reserves a workspace for
- * SPIKE_DEFAULT_MAX_B rows on the current device.  On success *out_handle
- * is set; on failure it is set to NULL. */
+ * SPIKE_DEFAULT_MAX_B rows on the current device and, when N % 64 == 0 and
+ * the copy stays below 2^31 bytes, packs the matrix-core copy of W
+ * (synchronous: it waits for the device before and after; if that memory
+ * cannot be allocated the handle simply has no matrix-core path).  On
+ * success *out_handle is set; on failure it is set to NULL. */
 int spike_proj_create(const int8_t *W_int8_colmajor, const float *scale_fp32, int32_t K, int32_t N,
                       spike_proj_t *out_handle);
 
@@ -76,7 +82,11 @@ int spike_proj_reserve(spike_proj_t h, int32_t max_B);
  * `stream` (a hipStream_t; NULL means the default stream).  B = 0 is a
  * no-op; 0 <= B <= the reserved max_B.  Dispatches to the active-column
  * gather (decode-sized B) or to the dense i8 matrix-core contraction over
- * the 0/1 spike matrix (prefill-sized B); both give identical bits. */
+ * the 0/1 spike matrix (batches from SPIKE_TUNE_MFMA_MIN_B rows, where the
+ * handle has the matrix-core copy of W); both give identical bits.  With
+ * SPIKE_PATH_MFMA forced on a handle without that copy, or for more rows
+ * than 31-bit offsets into the mask can address, it returns
+ * SPIKE_EUNSUPPORTED. */
 int spike_proj_forward(spike_proj_t h, const uint64_t *spike_bitmask, int32_t B, float *out_fp32,
                        void *stream);
 

@@ -153,8 +153,9 @@ struct spike_proj {
     int32_t* ws = nullptr;         // [max_B][N] INT32, zero between calls
     uint32_t* counters = nullptr;  // [max_B][counter_stride], zero between calls
     int32_t counter_stride = 0;
-    int32_t* parts = nullptr;      // partial tiles of the matrix-core K-split
-    int64_t parts_capacity = 0;    // INT32 entries: kMfmaMaxSplits * min(max_B, 64) * N
+    int8_t* packed = nullptr;      // matrix-core operand copy of W (null: no matrix-core path)
+    int32_t* parts = nullptr;      // partial tiles of the matrix-core K-split (null if N is too large)
+    int64_t parts_capacity = 0;    // INT32 entries: kMfmaMaxSplits * 64 * N
     int path = SPIKE_PATH_AUTO;
     int slice_words = 0;  // 0 = automatic
     int max_slices = 16;
@@ -210,7 +211,10 @@ int alloc_workspace(spike_proj* h, int32_t max_B)
     const size_t ws_bytes = (size_t)max_B * h->N * sizeof(int32_t);
     const int32_t stride = (int32_t)((h->N + kMinTile - 1) / kMinTile);
     const size_t ctr_bytes = (size_t)max_B * stride * sizeof(uint32_t);
-    const int64_t parts_cap = (int64_t)spk::kMfmaMaxSplits * std::min(max_B, spk::kMfmaSplitRows) * h->N;
+    // partial tiles of a matrix-core K-split: only where one buffer resource
+    // can address them (N < 2^20)
+    const int64_t parts_cap = (int64_t)spk::kMfmaMaxSplits * spk::kMfmaRows * h->N;
+    const bool want_parts = parts_cap * (int64_t)sizeof(int32_t) < (1ll << 31);
     int32_t* ws = nullptr;
     uint32_t* ctr = nullptr;
     int32_t* parts = nullptr;
@@ -218,7 +222,7 @@ int alloc_workspace(spike_proj* h, int32_t max_B)
     if (e != hipSuccess)
         return fail(SPIKE_ENOMEM, "workspace allocation of %zu bytes failed: %s", ws_bytes, hipGetErrorString(e));
     e = hipMalloc(&ctr, ctr_bytes);
-    if (e == hipSuccess)
+    if (e == hipSuccess && want_parts)
         e = hipMalloc(&parts, (size_t)parts_cap * sizeof(int32_t));
     if (e != hipSuccess) {
         (void)hipFree(ws);
@@ -244,7 +248,7 @@ int alloc_workspace(spike_proj* h, int32_t max_B)
     h->counters = ctr;
     h->counter_stride = stride;
     h->parts = parts;
-    h->parts_capacity = parts_cap;
+    h->parts_capacity = want_parts ? parts_cap : 0;
     h->max_B = max_B;
     return SPIKE_OK;
 }
@@ -327,13 +331,51 @@ int launch_gather(const spike_proj* h, const uint64_t* mask, int32_t B, float* o
     return e == hipSuccess ? SPIKE_OK : hip_fail(e, "gather launch");
 }
 
+// The matrix-core kernel addresses the B rows of spike words (plus the
+// padding rows of the last tile) with 31-bit byte offsets.
+bool mfma_rows_fit(const spike_proj* h, int32_t B)
+{
+    const int64_t rows = ((int64_t)B + spk::kMfmaRows - 1) / spk::kMfmaRows * spk::kMfmaRows;
+    return rows * h->wpr * (int64_t)sizeof(uint64_t) < (1ll << 31);
+}
+
 bool use_mfma(const spike_proj* h, int32_t B)
 {
     if (h->path == SPIKE_PATH_MFMA)
         return true;
     if (h->path == SPIKE_PATH_GATHER)
         return false;
-    return spk::mfma_supported(h->K, h->N, h->W) && B >= h->mfma_min_b;
+    return h->packed && B >= h->mfma_min_b && mfma_rows_fit(h, B);
+}
+
+// Packed operand copy of W for the matrix cores (layout in mfma.hpp), made
+// once; null where the shape has no matrix-core path or memory is short.
+int make_packed(spike_proj* h)
+{
+    if (!spk::mfma_supported(h->K, h->N))
+        return SPIKE_OK;
+    const int64_t bytes = spk::mfma_packed_bytes(h->K, h->N);
+    int8_t* P = nullptr;
+    if (hipMalloc(&P, (size_t)bytes) != hipSuccess) {
+        (void)hipGetLastError();  // no matrix-core path for this handle; the gather serves every B
+        return SPIKE_OK;
+    }
+    const int64_t chunks = bytes / 16;
+    const int64_t blocks = (chunks + spk::kPackBlock - 1) / spk::kPackBlock;
+    hipError_t e = hipDeviceSynchronize();  // W may still be in flight on any stream
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(spk::k_mfma_pack, dim3((unsigned)blocks), dim3(spk::kPackBlock), 0, nullptr, h->W, h->K,
+                           h->N, h->wpr, P, chunks);
+        e = hipGetLastError();
+    }
+    if (e == hipSuccess)
+        e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+        (void)hipFree(P);
+        return hip_fail(e, "packing the matrix-core copy of W");
+    }
+    h->packed = P;
+    return SPIKE_OK;
 }
 
 template <bool ACC>
@@ -351,17 +393,22 @@ int forward_impl(spike_proj* h, const uint64_t* mask, int32_t B, float* out, int
         return rc;
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (use_mfma(h, B)) {
-        if (!spk::mfma_supported(h->K, h->N, h->W))
-            return fail(SPIKE_EUNSUPPORTED, "matrix-core path needs N %% %d == 0 and a %d-byte aligned W",
-                        spk::kMfmaNAlign, spk::kMfmaNAlign);
+        if (!h->packed)
+            return fail(SPIKE_EUNSUPPORTED, "no matrix-core copy of W: it needs N %% %d == 0, fewer than 2^31 "
+                        "packed bytes and the memory for them", spk::kMfmaNAlign);
+        if (!mfma_rows_fit(h, B))
+            return fail(SPIKE_EUNSUPPORTED, "matrix-core path: %d rows of %d mask words exceed 31-bit offsets", B,
+                        h->wpr);
         int wps = 0;
         const int n_splits = spk::mfma_splits(h->K, h->N, B, h->mfma_split_words, &wps);
-        if (n_splits > 1 && (B > spk::kMfmaSplitRows || (int64_t)n_splits * B * h->N > h->parts_capacity))
-            return fail(SPIKE_EUNSUPPORTED, "matrix-core K-split of %d needs B <= %d and %lld partial entries "
-                        "(have %lld)", n_splits, spk::kMfmaSplitRows, (long long)n_splits * B * h->N,
-                        (long long)h->parts_capacity);
-        const hipError_t e = spk::launch_mfma(h->W, h->scale, h->K, h->N, mask, B, wps, n_splits, h->mfma_waves,
-                                              h->mfma_depth, h->parts, h->counters, out, acc, ACC, st);
+        const int64_t need = (int64_t)n_splits * spk::kMfmaRows * h->N;
+        if (n_splits > 1 && (n_splits > spk::kMfmaMaxSplits || B > spk::kMfmaSplitRows || need > h->parts_capacity))
+            return fail(SPIKE_EUNSUPPORTED, "matrix-core K-split of %d needs at most %d splits, B <= %d and %lld "
+                        "partial entries (have %lld)", n_splits, spk::kMfmaMaxSplits, spk::kMfmaSplitRows,
+                        (long long)need, (long long)h->parts_capacity);
+        const hipError_t e = spk::launch_mfma(h->packed, h->scale, h->K, h->N, mask, B, wps, n_splits,
+                                              h->mfma_waves, h->mfma_depth, h->parts, h->counters, out, acc, ACC,
+                                              st);
         return e == hipSuccess ? SPIKE_OK : hip_fail(e, "matrix-core launch");
     }
     return launch_gather<ACC>(h, mask, B, out, acc, st);
@@ -414,6 +461,14 @@ int spike_proj_create(const int8_t* W, const float* scale, int32_t K, int32_t N,
         delete h;
         return rc;
     }
+    if (int rc = make_packed(h)) {
+        (void)hipFree(h->ws);
+        (void)hipFree(h->counters);
+        if (h->parts)
+            (void)hipFree(h->parts);
+        delete h;
+        return rc;
+    }
     *out_handle = h;
     return SPIKE_OK;
 }
@@ -459,6 +514,8 @@ int spike_proj_destroy(spike_proj_t h)
         (void)hipFree(h->counters);
     if (h->parts)
         (void)hipFree(h->parts);
+    if (h->packed)
+        (void)hipFree(h->packed);
     delete h;
     return rc;
 }

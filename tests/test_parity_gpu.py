@@ -530,6 +530,34 @@ def test_matrix_core_rejects_unaligned_N(sp):
     assert_parity(sp, h, p["W"], p["scale"], p["masks"])
 
 
+@pytest.mark.parametrize("K", [100, 4097])
+def test_matrix_core_padding_junk_and_unaligned_weights(sp, K):
+    """Spike bits past K are ignored on the matrix-core path (they meet the
+    zero padding of its packed weight copy), and W needs no alignment there:
+    the copy is made once, at create, from a W that starts at an odd byte."""
+    N, B = 192, 70
+    p = wl.small_problem(K, N, B, 0.2, seed=K)
+    masks = p["masks"].copy()
+    masks[:, -1] |= np.uint64((~((1 << (K % 64)) - 1)) & 0xFFFFFFFFFFFFFFFF)
+    buf = torch.zeros(K * N + 1, dtype=torch.int8, device="cuda")
+    buf[1:].copy_(torch.from_numpy(p["W"].reshape(-1)))
+    Wd, sd = buf[1:].view(K, N), dev(p["scale"])
+    h = sp.spike_proj_create(Wd, sd)
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
+    assert_parity(sp, h, p["W"], p["scale"], masks)  # two row tiles
+    wpr = wl.words_per_row(K)
+    for wps in (0, -(-wpr // 8), -(-wpr // 3)):  # automatic, 8 and 3 K-splits (one row tile)
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_SPLIT_WORDS, wps)
+        assert_parity(sp, h, p["W"], p["scale"], masks[:64])
+        assert_parity(sp, h, p["W"], p["scale"], masks[:5])
+    # the packed copy is taken at create: later writes to W are not seen by
+    # the matrix cores (W is borrowed read-only for the handle's lifetime)
+    Wd.zero_()
+    torch.cuda.synchronize()
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_SPLIT_WORDS, 0)
+    assert_parity(sp, h, p["W"], p["scale"], masks)
+
+
 def test_paths_agree_on_prefill_and_padding_junk(sp):
     d = wl.prefill_projection(B=200)
     masks = d["masks"].copy()
