@@ -28,11 +28,12 @@
  * unchanged until destroy()).  The handle owns a small INT32 workspace of
  * max_B * N entries plus completion counters; the kernels leave it zeroed
  * after every call, so forward() performs no allocation, memset or host
- * synchronisation and can be captured into a HIP graph.  When N % 64 == 0
+ * synchronisation and can be captured into a HIP graph.  When N % 16 == 0
  * the handle also owns a copy of W in the matrix cores' operand order
- * (ceil(K/64) * 64 * N bytes, made once by create(); the matrix-core path
- * reads only that copy, so W must not change after create()).  A handle
- * must not run on two streams at the same time (its workspace is shared).
+ * (ceil(K/64) * 64 * N bytes, made by create() and kept while the reserved
+ * batch is at least the matrix-core minimum; the matrix-core path reads
+ * only that copy, so W must not change after it is made).  A handle must
+ * not run on two streams at the same time (its workspace is shared).
  *
  * Errors: every entry point returns SPIKE_OK (0) or a negative code;
  * spike_proj_last_error() returns a message for the calling thread's last
@@ -65,7 +66,7 @@ typedef struct spike_stream *spike_stream_t;
  * FP32 scales [N] (Sec. 2.2: binary-input projections are stored
  * column-major; Sec. 2.3: one scale per output channel).  1 <= K <=
  * SPIKE_MAX_K, 1 <= N <= SPIKE_MAX_N.  Reserves a workspace for
- * SPIKE_DEFAULT_MAX_B rows on the current device and, when N % 64 == 0 and
+ * SPIKE_DEFAULT_MAX_B rows on the current device and, when N % 16 == 0 and
  * the copy stays below 2^31 bytes, packs the matrix-core copy of W
  * (synchronous: it waits for the device before and after; if that memory
  * cannot be allocated the handle simply has no matrix-core path).  On
@@ -74,8 +75,12 @@ int spike_proj_create(const int8_t *W_int8_colmajor, const float *scale_fp32, in
                       spike_proj_t *out_handle);
 
 /* Resize the workspace so that forward() accepts up to max_B rows
- * (1 <= max_B <= 65535).  Allocates; call it outside graph capture and
- * while no forward() of this handle is in flight. */
+ * (1 <= max_B <= 65535).  A max_B below the matrix-core minimum batch
+ * (SPIKE_TUNE_MFMA_MIN_B, default 5) also frees the matrix-core copy of W,
+ * so handles that only ever run batch-1 calls hold no second copy; a larger
+ * max_B makes the copy again where the shape allows it.  Allocates and
+ * synchronises the device; call it outside graph capture and while no
+ * forward() of this handle is in flight. */
 int spike_proj_reserve(spike_proj_t h, int32_t max_B);
 
 /* y = Eq. (sparse) for B spike rows: out[b*N + n].  Asynchronous on
@@ -83,9 +88,11 @@ int spike_proj_reserve(spike_proj_t h, int32_t max_B);
  * no-op; 0 <= B <= the reserved max_B.  Dispatches to the active-column
  * gather (decode-sized B) or to the dense i8 matrix-core contraction over
  * the 0/1 spike matrix (batches from SPIKE_TUNE_MFMA_MIN_B rows, where the
- * handle has the matrix-core copy of W); both give identical bits.  With
- * SPIKE_PATH_MFMA forced on a handle without that copy, or for more rows
- * than 31-bit offsets into the mask can address, it returns
+ * handle has the matrix-core copy of W and the matrix-core launch plan can
+ * run; otherwise the gather serves the call); both give identical bits.
+ * With SPIKE_PATH_MFMA forced where the matrix-core plan cannot run (no
+ * copy of W, a tuned plan that is not instantiated or does not fit, more
+ * rows than 31-bit offsets into the mask can address) it returns
  * SPIKE_EUNSUPPORTED. */
 int spike_proj_forward(spike_proj_t h, const uint64_t *spike_bitmask, int32_t B, float *out_fp32,
                        void *stream);
@@ -120,13 +127,20 @@ int spike_proj_destroy(spike_proj_t h);
  *   SPIKE_TUNE_XCD_SPREAD   streams only: 1 = plain unit order; 8 = keep the
  *                           tiles of one (token, projection) on one XCD
  *   SPIKE_TUNE_MFMA_WAVES   waves per workgroup of the matrix-core path, which
- *                           share one tile's K range: 0 = automatic, 4, 8
+ *                           share one tile's K range: 0 = automatic, 4, 8, 16
  *   SPIKE_TUNE_MFMA_DEPTH   k-steps of weights in flight per wave of the
- *                           matrix-core path: 0 = automatic, 1, 2, 4
- *   SPIKE_TUNE_MFMA_SPLIT_WORDS  mask words per K-split of the matrix-core
- *                           path (0 = automatic).  Splits exist only for
- *                           B <= 64 and at most 8 of them; a forward that
- *                           would need more returns SPIKE_EUNSUPPORTED.
+ *                           matrix-core path: 0 = automatic, 2, 4, 8, 12 (when a
+ *                           wave has at most that many k-steps, all of its
+ *                           loads are issued at once)
+ *   SPIKE_TUNE_MFMA_ROW_TILE  16-row subtiles per matrix-core workgroup:
+ *                           0 = automatic, 1, 2, 4, 8
+ *   SPIKE_TUNE_MFMA_COL_SETS  16-channel sets per matrix-core workgroup:
+ *                           0 = automatic, 1, 2, 3, 4, 6
+ *                           Only the matrix-core plans the library
+ *                           instantiates run; forcing SPIKE_PATH_MFMA with
+ *                           another combination makes forward() return
+ *                           SPIKE_EUNSUPPORTED (AUTO falls back to the
+ *                           gather).
  * Returns SPIKE_EINVAL for an unknown key or a value out of range.
  */
 #define SPIKE_TUNE_PATH 1
@@ -138,8 +152,9 @@ int spike_proj_destroy(spike_proj_t h);
 #define SPIKE_TUNE_TILES_PER_UNIT 7
 #define SPIKE_TUNE_XCD_SPREAD 8
 #define SPIKE_TUNE_MFMA_WAVES 9
-#define SPIKE_TUNE_MFMA_SPLIT_WORDS 10
 #define SPIKE_TUNE_MFMA_DEPTH 11
+#define SPIKE_TUNE_MFMA_ROW_TILE 12
+#define SPIKE_TUNE_MFMA_COL_SETS 13
 #define SPIKE_SHAPE(V, LG, U, BLOCK) ((V) | ((LG) << 5) | ((U) << 15) | (((BLOCK) / 64) << 20))
 #define SPIKE_SHAPE_NT (1 << 25) /* or-ed into a shape code: nontemporal weight loads */
 #define SPIKE_PATH_AUTO 0
@@ -151,6 +166,20 @@ int spike_proj_tune(spike_proj_t h, int32_t key, int32_t value);
  * to `codes` (host memory; may be NULL when cap is 0) and returns how many
  * exist. */
 int spike_proj_shapes(int32_t *codes, int32_t cap);
+
+/* The matrix-core plans this build instantiates, as codes
+ * rt | cs << 4 | kw << 8 | d << 16 | preload << 24 (16-row subtiles and
+ * 16-channel sets per workgroup, waves, k-steps of weights in flight per
+ * wave, all loads issued at once): writes up to `cap` codes to `codes`
+ * (host memory; may be NULL when cap is 0) and returns how many exist. */
+int spike_mfma_plans(int32_t *codes, int32_t cap);
+
+/* Which path a forward() of B rows takes on a handle created for a K x N
+ * projection with default tuning and enough reserved rows (assuming the
+ * matrix-core copy of W could be allocated): *path receives
+ * SPIKE_PATH_GATHER or SPIKE_PATH_MFMA, *plan the matrix-core plan code (as
+ * in spike_mfma_plans) or 0.  Host-only: no device is touched. */
+int spike_proj_plan_query(int32_t K, int32_t N, int32_t B, int32_t *path, int32_t *plan);
 
 /* Active-index extraction (Sec. 2.2, A = {k : x_k = 1}) as a standalone
  * kernel.  For each row b < B writes the ascending active indices to
@@ -188,7 +217,7 @@ int spike_stream_destroy(spike_stream_t s);
 const char *spike_proj_last_error(void);
 
 /* ABI version of this header. */
-#define SPIKE_PROJ_ABI_VERSION 1
+#define SPIKE_PROJ_ABI_VERSION 2
 int spike_proj_abi_version(void);
 
 #ifdef __cplusplus

@@ -17,7 +17,7 @@ from .build import LIB
 SPIKE_OK, SPIKE_EINVAL, SPIKE_EHIP, SPIKE_ENOMEM, SPIKE_EUNSUPPORTED = 0, -1, -2, -3, -4
 SPIKE_TUNE_PATH, SPIKE_TUNE_SLICE_WORDS, SPIKE_TUNE_MFMA_MIN_B, SPIKE_TUNE_VEC, SPIKE_TUNE_MAX_SLICES = 1, 2, 3, 4, 5
 SPIKE_TUNE_SHAPE, SPIKE_TUNE_TILES_PER_UNIT, SPIKE_TUNE_XCD_SPREAD, SPIKE_TUNE_MFMA_WAVES = 6, 7, 8, 9
-SPIKE_TUNE_MFMA_SPLIT_WORDS, SPIKE_TUNE_MFMA_DEPTH = 10, 11
+SPIKE_TUNE_MFMA_DEPTH, SPIKE_TUNE_MFMA_ROW_TILE, SPIKE_TUNE_MFMA_COL_SETS = 11, 12, 13
 SPIKE_SHAPE_NT = 1 << 25
 SPIKE_PATH_AUTO, SPIKE_PATH_GATHER, SPIKE_PATH_MFMA = 0, 1, 2
 SPIKE_DEFAULT_MAX_B = 512
@@ -31,7 +31,7 @@ EXPORTED = (
     "spike_proj_create", "spike_proj_reserve", "spike_proj_forward", "spike_proj_forward_acc",
     "spike_proj_destroy", "spike_proj_tune", "spike_compact", "spike_stack_forward",
     "spike_stream_create", "spike_stream_forward", "spike_stream_tune", "spike_stream_destroy",
-    "spike_proj_last_error", "spike_proj_shapes",
+    "spike_proj_last_error", "spike_proj_shapes", "spike_mfma_plans", "spike_proj_plan_query",
     "spike_proj_abi_version",
 )
 
@@ -55,6 +55,8 @@ _sig = {
     "spike_stream_destroy": [_p],
     "spike_proj_abi_version": [],
     "spike_proj_shapes": [_p, _i32],
+    "spike_mfma_plans": [_p, _i32],
+    "spike_proj_plan_query": [_i32, _i32, _i32, _p, _p],
 }
 for _name, _args in _sig.items():
     getattr(_lib, _name).argtypes = _args
@@ -230,6 +232,27 @@ def spike_proj_shapes() -> list:
     buf = (ctypes.c_int32 * n)()
     _lib.spike_proj_shapes(buf, n)
     return list(buf)
+
+
+def spike_mfma_plans() -> list:
+    """Matrix-core plans instantiated by the library, as dicts."""
+    n = _lib.spike_mfma_plans(None, 0)
+    buf = (ctypes.c_int32 * n)()
+    _lib.spike_mfma_plans(buf, n)
+    return [decode_plan(c) for c in buf]
+
+
+def decode_plan(code: int) -> dict:
+    return {"rt": code & 15, "cs": (code >> 4) & 15, "kw": (code >> 8) & 255, "d": (code >> 16) & 255,
+            "preload": bool((code >> 24) & 1)}
+
+
+def spike_proj_plan_query(K: int, N: int, B: int):
+    """(path, plan dict or None) that AUTO takes for B rows of a K x N projection."""
+    path, plan = ctypes.c_int32(), ctypes.c_int32()
+    _check(_lib.spike_proj_plan_query(int(K), int(N), int(B), ctypes.byref(path), ctypes.byref(plan)),
+           "spike_proj_plan_query")
+    return path.value, (decode_plan(plan.value) if plan.value else None)
 
 
 def spike_proj_abi_version() -> int:

@@ -142,6 +142,9 @@ constexpr int kLatencySliceWords = 24;
 
 constexpr int kMinTile = 32;  // smallest tile of any shape: sizes the counter array
 
+// Smallest batch that AUTO sends to the matrix cores.
+constexpr int kDefaultMfmaMinB = 5;
+
 }  // namespace
 
 struct spike_proj {
@@ -154,18 +157,17 @@ struct spike_proj {
     uint32_t* counters = nullptr;  // [max_B][counter_stride], zero between calls
     int32_t counter_stride = 0;
     int8_t* packed = nullptr;      // matrix-core operand copy of W (null: no matrix-core path)
-    int32_t* parts = nullptr;      // partial tiles of the matrix-core K-split (null if N is too large)
-    int64_t parts_capacity = 0;    // INT32 entries: kMfmaMaxSplits * 64 * N
     int path = SPIKE_PATH_AUTO;
     int slice_words = 0;  // 0 = automatic
     int max_slices = 16;
     const ShapeEntry* shape = nullptr;  // throughput shape (B above the latency range)
     bool shape_pinned = false;          // set by SPIKE_TUNE_SHAPE / _VEC: used for every B
     int tiles_per_unit = 1;
-    int mfma_min_b = 5;  // measured crossover: the matrix cores win from 8 rows, tie at 4
-    int mfma_waves = 0;        // 0 = automatic
-    int mfma_split_words = 0;  // 0 = automatic
-    int mfma_depth = 0;        // 0 = automatic
+    int mfma_min_b = kDefaultMfmaMinB;
+    int mfma_waves = 0;      // 0 = automatic
+    int mfma_depth = 0;      // 0 = automatic
+    int mfma_row_tile = 0;   // 16-row subtiles per workgroup, 0 = automatic
+    int mfma_col_sets = 0;   // 16-channel sets per workgroup, 0 = automatic
 };
 
 struct spike_stream {
@@ -211,23 +213,14 @@ int alloc_workspace(spike_proj* h, int32_t max_B)
     const size_t ws_bytes = (size_t)max_B * h->N * sizeof(int32_t);
     const int32_t stride = (int32_t)((h->N + kMinTile - 1) / kMinTile);
     const size_t ctr_bytes = (size_t)max_B * stride * sizeof(uint32_t);
-    // partial tiles of a matrix-core K-split: only where one buffer resource
-    // can address them (N < 2^20)
-    const int64_t parts_cap = (int64_t)spk::kMfmaMaxSplits * spk::kMfmaRows * h->N;
-    const bool want_parts = parts_cap * (int64_t)sizeof(int32_t) < (1ll << 31);
     int32_t* ws = nullptr;
     uint32_t* ctr = nullptr;
-    int32_t* parts = nullptr;
     hipError_t e = hipMalloc(&ws, ws_bytes);
     if (e != hipSuccess)
         return fail(SPIKE_ENOMEM, "workspace allocation of %zu bytes failed: %s", ws_bytes, hipGetErrorString(e));
     e = hipMalloc(&ctr, ctr_bytes);
-    if (e == hipSuccess && want_parts)
-        e = hipMalloc(&parts, (size_t)parts_cap * sizeof(int32_t));
     if (e != hipSuccess) {
         (void)hipFree(ws);
-        if (ctr)
-            (void)hipFree(ctr);
         return fail(SPIKE_ENOMEM, "workspace allocation failed: %s", hipGetErrorString(e));
     }
     // Zeroed once here; the kernels leave both zeroed after every call.
@@ -235,20 +228,15 @@ int alloc_workspace(spike_proj* h, int32_t max_B)
         (e = hipDeviceSynchronize()) != hipSuccess) {
         (void)hipFree(ws);
         (void)hipFree(ctr);
-        (void)hipFree(parts);
         return hip_fail(e, "workspace initialisation");
     }
     if (h->ws)
         (void)hipFree(h->ws);
     if (h->counters)
         (void)hipFree(h->counters);
-    if (h->parts)
-        (void)hipFree(h->parts);
     h->ws = ws;
     h->counters = ctr;
     h->counter_stride = stride;
-    h->parts = parts;
-    h->parts_capacity = want_parts ? parts_cap : 0;
     h->max_B = max_B;
     return SPIKE_OK;
 }
@@ -331,12 +319,33 @@ int launch_gather(const spike_proj* h, const uint64_t* mask, int32_t B, float* o
     return e == hipSuccess ? SPIKE_OK : hip_fail(e, "gather launch");
 }
 
-// The matrix-core kernel addresses the B rows of spike words (plus the
-// padding rows of the last tile) with 31-bit byte offsets.
-bool mfma_rows_fit(const spike_proj* h, int32_t B)
+spk::MfmaPlan mfma_plan_of(const spike_proj* h, int32_t B)
 {
-    const int64_t rows = ((int64_t)B + spk::kMfmaRows - 1) / spk::kMfmaRows * spk::kMfmaRows;
-    return rows * h->wpr * (int64_t)sizeof(uint64_t) < (1ll << 31);
+    return spk::mfma_plan(h->K, h->N, B, h->mfma_row_tile, h->mfma_col_sets, h->mfma_waves, h->mfma_depth);
+}
+
+// Why the matrix-core path cannot serve B rows of a K x N projection with
+// plan p (null: it can).  The kernel addresses the spike words of its row
+// tiles (including the padding rows of the last one) with 31-bit offsets.
+const char* mfma_refusal(int32_t K, int32_t N, bool has_copy, int32_t B, const spk::MfmaPlan& p)
+{
+    if (!has_copy)
+        return "the handle has no matrix-core copy of W (it needs N % 16 == 0, fewer than 2^31 packed bytes, "
+               "a reserved batch of at least the matrix-core minimum and the memory for the copy)";
+    if (const char* why = spk::mfma_plan_check(p, K, N))
+        return why;
+    const int64_t tile = 16ll * p.rt;
+    const int64_t rows = ((int64_t)B + tile - 1) / tile * tile;
+    if (rows * words_per_row(K) * (int64_t)sizeof(uint64_t) >= (1ll << 31))
+        return "the spike rows exceed 31-bit offsets";
+    return nullptr;
+}
+
+// AUTO sends batches from mfma_min_b rows to the matrix cores whenever
+// their plan can run, and everything else to the gather.
+bool auto_uses_mfma(int32_t K, int32_t N, bool has_copy, int32_t B, int min_b, const spk::MfmaPlan& p)
+{
+    return B >= min_b && mfma_refusal(K, N, has_copy, B, p) == nullptr;
 }
 
 bool use_mfma(const spike_proj* h, int32_t B)
@@ -345,7 +354,7 @@ bool use_mfma(const spike_proj* h, int32_t B)
         return true;
     if (h->path == SPIKE_PATH_GATHER)
         return false;
-    return h->packed && B >= h->mfma_min_b && mfma_rows_fit(h, B);
+    return auto_uses_mfma(h->K, h->N, h->packed != nullptr, B, h->mfma_min_b, mfma_plan_of(h, B));
 }
 
 // Packed operand copy of W for the matrix cores (layout in mfma.hpp), made
@@ -393,22 +402,11 @@ int forward_impl(spike_proj* h, const uint64_t* mask, int32_t B, float* out, int
         return rc;
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (use_mfma(h, B)) {
-        if (!h->packed)
-            return fail(SPIKE_EUNSUPPORTED, "no matrix-core copy of W: it needs N %% %d == 0, fewer than 2^31 "
-                        "packed bytes and the memory for them", spk::kMfmaNAlign);
-        if (!mfma_rows_fit(h, B))
-            return fail(SPIKE_EUNSUPPORTED, "matrix-core path: %d rows of %d mask words exceed 31-bit offsets", B,
-                        h->wpr);
-        int wps = 0;
-        const int n_splits = spk::mfma_splits(h->K, h->N, B, h->mfma_split_words, &wps);
-        const int64_t need = (int64_t)n_splits * spk::kMfmaRows * h->N;
-        if (n_splits > 1 && (n_splits > spk::kMfmaMaxSplits || B > spk::kMfmaSplitRows || need > h->parts_capacity))
-            return fail(SPIKE_EUNSUPPORTED, "matrix-core K-split of %d needs at most %d splits, B <= %d and %lld "
-                        "partial entries (have %lld)", n_splits, spk::kMfmaMaxSplits, spk::kMfmaSplitRows,
-                        (long long)need, (long long)h->parts_capacity);
-        const hipError_t e = spk::launch_mfma(h->packed, h->scale, h->K, h->N, mask, B, wps, n_splits,
-                                              h->mfma_waves, h->mfma_depth, h->parts, h->counters, out, acc, ACC,
-                                              st);
+        const spk::MfmaPlan p = mfma_plan_of(h, B);
+        if (const char* why = mfma_refusal(h->K, h->N, h->packed != nullptr, B, p))
+            return fail(SPIKE_EUNSUPPORTED, "matrix-core path for B = %d, K = %d, N = %d (row tile %d, channel sets "
+                        "%d, waves %d, depth %d): %s", B, h->K, h->N, p.rt, p.cs, p.kw, p.d, why);
+        const hipError_t e = spk::launch_mfma(p, h->packed, h->scale, h->K, h->N, mask, B, out, acc, ACC, st);
         return e == hipSuccess ? SPIKE_OK : hip_fail(e, "matrix-core launch");
     }
     return launch_gather<ACC>(h, mask, B, out, acc, st);
@@ -464,8 +462,6 @@ int spike_proj_create(const int8_t* W, const float* scale, int32_t K, int32_t N,
     if (int rc = make_packed(h)) {
         (void)hipFree(h->ws);
         (void)hipFree(h->counters);
-        if (h->parts)
-            (void)hipFree(h->parts);
         delete h;
         return rc;
     }
@@ -480,14 +476,24 @@ int spike_proj_reserve(spike_proj_t h, int32_t max_B)
         return fail(SPIKE_EINVAL, "null handle");
     if (max_B < 1 || max_B > 65535)
         return fail(SPIKE_EINVAL, "max_B = %d outside [1, 65535]", max_B);
-    if (max_B == h->max_B)
+    if (max_B == h->max_B && (max_B < h->mfma_min_b || h->packed || !spk::mfma_supported(h->K, h->N)))
         return SPIKE_OK;
     if (int rc = check_device(h->device))
         return rc;
     hipError_t e = hipDeviceSynchronize();
     if (e != hipSuccess)
         return hip_fail(e, "hipDeviceSynchronize");
-    return alloc_workspace(h, max_B);
+    if (int rc = alloc_workspace(h, max_B))
+        return rc;
+    // The matrix-core copy of W is kept only while batches that would use it
+    // can be run: fewer reserved rows than the matrix-core minimum free it.
+    if (max_B < h->mfma_min_b) {
+        if (h->packed)
+            (void)hipFree(h->packed);
+        h->packed = nullptr;
+        return SPIKE_OK;
+    }
+    return h->packed ? SPIKE_OK : make_packed(h);
 }
 
 int spike_proj_forward(spike_proj_t h, const uint64_t* mask, int32_t B, float* out, void* stream)
@@ -512,8 +518,6 @@ int spike_proj_destroy(spike_proj_t h)
         (void)hipFree(h->ws);
     if (h->counters)
         (void)hipFree(h->counters);
-    if (h->parts)
-        (void)hipFree(h->parts);
     if (h->packed)
         (void)hipFree(h->packed);
     delete h;
@@ -566,20 +570,25 @@ int spike_proj_tune(spike_proj_t h, int32_t key, int32_t value)
             return fail(SPIKE_EINVAL, "tiles per unit %d outside [1, 4096]", value);
         h->tiles_per_unit = value;
         return SPIKE_OK;
-    case SPIKE_TUNE_MFMA_SPLIT_WORDS:
-        if (value < 0)
-            return fail(SPIKE_EINVAL, "matrix-core split words must be >= 0, got %d", value);
-        h->mfma_split_words = value;
-        return SPIKE_OK;
     case SPIKE_TUNE_MFMA_DEPTH:
-        if (value != 0 && value != 1 && value != 2 && value != 4)
-            return fail(SPIKE_EINVAL, "matrix-core depth must be 0, 1, 2 or 4, got %d", value);
+        if (value != 0 && value != 2 && value != 4 && value != 8 && value != 12)
+            return fail(SPIKE_EINVAL, "matrix-core depth must be 0, 2, 4, 8 or 12, got %d", value);
         h->mfma_depth = value;
         return SPIKE_OK;
     case SPIKE_TUNE_MFMA_WAVES:
-        if (value != 0 && value != 4 && value != 8)
-            return fail(SPIKE_EINVAL, "matrix-core waves per workgroup must be 0, 4 or 8, got %d", value);
+        if (value != 0 && value != 1 && value != 2 && value != 4 && value != 8 && value != 16)
+            return fail(SPIKE_EINVAL, "matrix-core waves per workgroup must be 0, 1, 2, 4, 8 or 16, got %d", value);
         h->mfma_waves = value;
+        return SPIKE_OK;
+    case SPIKE_TUNE_MFMA_ROW_TILE:
+        if (value != 0 && value != 1 && value != 2 && value != 4 && value != 8)
+            return fail(SPIKE_EINVAL, "matrix-core row subtiles must be 0, 1, 2, 4 or 8, got %d", value);
+        h->mfma_row_tile = value;
+        return SPIKE_OK;
+    case SPIKE_TUNE_MFMA_COL_SETS:
+        if (value < 0 || value > 6 || value == 5)
+            return fail(SPIKE_EINVAL, "matrix-core channel sets must be 0, 1, 2, 3, 4 or 6, got %d", value);
+        h->mfma_col_sets = value;
         return SPIKE_OK;
     default:
         return fail(SPIKE_EINVAL, "unknown tuning key %d", key);
@@ -806,6 +815,22 @@ int spike_proj_shapes(int32_t* codes, int32_t cap)
     for (int i = 0; i < n && i < cap && codes; ++i)
         codes[i] = kShapes[i].code;
     return n;
+}
+
+int spike_mfma_plans(int32_t* codes, int32_t cap) { return spk::mfma_plan_codes(codes, cap); }
+
+int spike_proj_plan_query(int32_t K, int32_t N, int32_t B, int32_t* path, int32_t* plan)
+{
+    g_last_error.clear();
+    if (!path || !plan)
+        return fail(SPIKE_EINVAL, "null output pointer");
+    if (K < 1 || K > SPIKE_MAX_K || N < 1 || N > SPIKE_MAX_N || B < 0)
+        return fail(SPIKE_EINVAL, "K = %d, N = %d or B = %d out of range", K, N, B);
+    const spk::MfmaPlan p = spk::mfma_plan(K, N, B, 0, 0, 0, 0);
+    const bool mf = auto_uses_mfma(K, N, spk::mfma_supported(K, N), B, kDefaultMfmaMinB, p);
+    *path = mf ? SPIKE_PATH_MFMA : SPIKE_PATH_GATHER;
+    *plan = mf ? spk::mfma_plan_code(p) : 0;
+    return SPIKE_OK;
 }
 
 const char* spike_proj_last_error(void) { return g_last_error.c_str(); }

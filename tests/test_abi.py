@@ -39,7 +39,7 @@ def test_library_exports_every_declared_symbol(sp):
 
 
 def test_abi_version(sp):
-    assert sp.spike_proj_abi_version() == 1
+    assert sp.spike_proj_abi_version() == 2
 
 
 def test_argument_validation_before_any_hip_call(sp):
@@ -77,3 +77,26 @@ def test_product_path_never_touches_the_oracle():
             assert "spike_oracle" not in text, path
     hdr = open(os.path.join(ROOT, "include", "spike_proj.h")).read()
     assert "oracle" not in hdr
+
+
+def test_automatic_matrix_core_plans_are_instantiated(sp):
+    """For every shape and batch the host-side planner sends to the matrix
+    cores, the plan is one the library instantiates; the decode shapes and
+    the prefill shape go where the design puts them (no GPU needed)."""
+    plans = {tuple(p.values()) for p in sp.spike_mfma_plans()}
+    for K in (1, 63, 64, 65, 100, 1000, 1536, 2048, 4097, 6144, 16384, 20000, 40000):
+        for N in (16, 64, 100, 192, 1536, 6144, 1 << 20):
+            for B in (1, 4, 5, 17, 64, 65, 130, 512, 4096):
+                path, plan = sp.spike_proj_plan_query(K, N, B)
+                if path == sp.SPIKE_PATH_MFMA:
+                    assert tuple(plan.values()) in plans, (K, N, B, plan)
+                    assert B >= 5 and N % 16 == 0
+                else:
+                    assert path == sp.SPIKE_PATH_GATHER
+    assert sp.spike_proj_plan_query(1536, 1536, 1)[0] == sp.SPIKE_PATH_GATHER
+    assert sp.spike_proj_plan_query(6144, 1536, 4)[0] == sp.SPIKE_PATH_GATHER
+    for K in (1536, 6144):
+        path, plan = sp.spike_proj_plan_query(K, 1536, 64)
+        assert path == sp.SPIKE_PATH_MFMA and plan["rt"] == 1
+    path, plan = sp.spike_proj_plan_query(6144, 1536, 512)
+    assert path == sp.SPIKE_PATH_MFMA and plan["rt"] == 4

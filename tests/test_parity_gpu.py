@@ -489,18 +489,63 @@ def test_stream_every_shape_and_xcd_spread(sp, stack):
 @pytest.mark.parametrize("K,N", [(100, 64), (1536, 1536), (4097, 192), (6144, 1024)])
 def test_matrix_core_path(sp, B, K, N):
     """The dense i8 matrix-core contraction over the 0/1 spike matrix gives the
-    oracle's bits, with and without K-splits, for ragged B and K."""
+    oracle's bits with its automatic plan and with 4, 8 and 16 waves, for
+    ragged B and K."""
     p = wl.small_problem(K, N, B, 0.15, seed=B * 7 + K)
     h, *_ = make(sp, p["W"], p["scale"])
     sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
+    assert_parity(sp, h, p["W"], p["scale"], p["masks"])
     wpr = wl.words_per_row(K)
-    # K-splits across workgroups exist for one row tile (B <= 64), at most 8
-    splits = (0, -(-wpr // 8), -(-wpr // 3), wpr) if B <= 64 else (0, wpr)
-    for wps in splits:
-        for waves in (0, 4, 8):
-            sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_SPLIT_WORDS, wps)
-            sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_WAVES, waves)
+    for waves in (4, 8, 16):
+        if waves > wpr:
+            continue
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_WAVES, waves)
+        try:
             assert_parity(sp, h, p["W"], p["scale"], p["masks"])
+        except sp.SpikeError as e:  # that wave count has no instantiated plan for this shape
+            assert e.code == sp.SPIKE_EUNSUPPORTED
+
+
+def plan_shape(plan, seed):
+    """A ragged shape that the given matrix-core plan can run: K past a
+    multiple of 64, B past a row-tile multiple, N over a number of tiles that
+    is not a multiple of 8 (plain tile order) for odd seeds."""
+    rt, cs, kw, d = plan["rt"], plan["cs"], plan["kw"], plan["d"]
+    if plan["preload"]:
+        wpr = max(kw, kw * d - 1)
+    else:
+        wpr = kw * d * 2 + 3
+    stage_words = (64 * 1024 - rt * cs * 1024) // (128 * rt)
+    wpr = min(wpr, stage_words - 1)
+    K = 64 * (wpr - 1) + 37
+    coltiles = 8 if seed % 2 == 0 else 5
+    N = 16 * cs * coltiles
+    B = 16 * rt + 16 * rt // 2 + 3
+    return K, N, B
+
+
+def test_every_matrix_core_plan(sp):
+    """Every instantiated matrix-core plan (tile height and width, waves,
+    weight depth, preloaded or ring) against the oracle, on a shape it runs."""
+    plans = sp.spike_mfma_plans()
+    assert len(plans) >= 30
+    for i, plan in enumerate(plans):
+        K, N, B = plan_shape(plan, i)
+        wpr = wl.words_per_row(K)
+        steps = -(-wpr // plan["kw"])
+        assert wpr >= plan["kw"] and (steps <= plan["d"]) == plan["preload"], (plan, K)
+        p = wl.small_problem(K, N, B, 0.2, seed=i)
+        masks = p["masks"].copy()
+        masks[:, -1] |= np.uint64((~((1 << (K % 64)) - 1)) & 0xFFFFFFFFFFFFFFFF)  # junk past K
+        h, *_ = make(sp, p["W"], p["scale"])
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_ROW_TILE, plan["rt"])
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_COL_SETS, plan["cs"])
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_WAVES, plan["kw"])
+        sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_DEPTH, plan["d"])
+        print(f"plan {plan} K={K} N={N} B={B}", flush=True)
+        assert_parity(sp, h, p["W"], p["scale"], masks)
+        h.close()
 
 
 def test_matrix_core_extremes(sp):
@@ -512,10 +557,10 @@ def test_matrix_core_extremes(sp):
     bits = np.ones((70, K), bool)
     bits[3] = False
     masks = wl.pack_bits(bits)
-    masks[:, -1] |= np.uint64(0)  # K is a multiple of 64: no padding bits
     h, *_ = make(sp, W, scale)
     sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
     assert_parity(sp, h, W, scale, masks)
+    assert_parity(sp, h, W, scale, masks[:9])
 
 
 def test_matrix_core_rejects_unaligned_N(sp):
@@ -528,6 +573,65 @@ def test_matrix_core_rejects_unaligned_N(sp):
     assert e.value.code == sp.SPIKE_EUNSUPPORTED
     sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_AUTO)  # AUTO falls back to the gather
     assert_parity(sp, h, p["W"], p["scale"], p["masks"])
+
+
+def test_auto_falls_back_when_the_plan_cannot_run(sp):
+    """A tuned matrix-core plan that is not instantiated is refused when the
+    matrix cores are forced, and AUTO serves the same call on the gather."""
+    p = wl.small_problem(1536, 1536, 40, 0.1, seed=11)
+    h, *_ = make(sp, p["W"], p["scale"])
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_ROW_TILE, 8)
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_COL_SETS, 6)
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
+    out = torch.empty((40, 1536), device="cuda")
+    with pytest.raises(sp.SpikeError) as e:
+        sp.spike_proj_forward(h, dmask(p["masks"]), 40, out)
+    assert e.value.code == sp.SPIKE_EUNSUPPORTED and "instantiated" in str(e.value)
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_AUTO)
+    assert_parity(sp, h, p["W"], p["scale"], p["masks"])
+
+
+def test_reserve_drops_and_remakes_the_matrix_core_copy(sp):
+    """reserve() below the matrix-core minimum frees the packed copy (the
+    matrix cores then refuse, AUTO uses the gather); a larger reserve makes it
+    again from W."""
+    p = wl.small_problem(1000, 256, 20, 0.2, seed=5)
+    h, *_ = make(sp, p["W"], p["scale"])
+    sp.spike_proj_reserve(h, 1)
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
+    out = torch.empty((1, 256), device="cuda")
+    with pytest.raises(sp.SpikeError) as e:
+        sp.spike_proj_forward(h, dmask(p["masks"][:1]), 1, out)
+    assert e.value.code == sp.SPIKE_EUNSUPPORTED
+    sp.spike_proj_reserve(h, 20)
+    assert_parity(sp, h, p["W"], p["scale"], p["masks"])
+
+
+def test_auto_path_at_a_million_channels(sp):
+    """K = 1600, N = 2^20, B = 10: AUTO runs this on the matrix cores (plan
+    query and result); 4096 sampled channels are checked against the oracle
+    on the same columns of W."""
+    K, N, B = 1600, 1 << 20, 10
+    path, plan = sp.spike_proj_plan_query(K, N, B)
+    assert path == sp.SPIKE_PATH_MFMA and plan is not None
+    rng = np.random.default_rng(77)
+    Wd = torch.randint(-127, 128, (K, N), dtype=torch.int8, device="cuda")
+    sd = torch.rand(N, device="cuda") * 9e-3 + 1e-3
+    bits = rng.random((B, K)) < 0.1
+    masks = wl.pack_bits(bits)
+    h = sp.spike_proj_create(Wd, sd)
+    out = torch.empty((B, N), device="cuda")
+    sp.spike_proj_forward(h, dmask(masks), B, out)
+    torch.cuda.synchronize()
+    sel = np.sort(rng.choice(N, 4096, replace=False))
+    sel_t = torch.from_numpy(sel).cuda()
+    Wsel = Wd[:, sel_t].cpu().numpy()
+    ssel = sd[sel_t].cpu().numpy()
+    ref = oracle.spike_forward(Wsel, ssel, masks, threads=8)
+    got = out[:, sel_t].cpu().numpy()
+    assert np.array_equal(bits32(got), bits32(ref))
+    h.close()
+    del Wd
 
 
 @pytest.mark.parametrize("K", [100, 4097])
@@ -544,55 +648,28 @@ def test_matrix_core_padding_junk_and_unaligned_weights(sp, K):
     Wd, sd = buf[1:].view(K, N), dev(p["scale"])
     h = sp.spike_proj_create(Wd, sd)
     sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
-    assert_parity(sp, h, p["W"], p["scale"], masks)  # two row tiles
-    wpr = wl.words_per_row(K)
-    for wps in (0, -(-wpr // 8), -(-wpr // 3)):  # automatic, 8 and 3 K-splits (one row tile)
-        sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_SPLIT_WORDS, wps)
-        assert_parity(sp, h, p["W"], p["scale"], masks[:64])
-        assert_parity(sp, h, p["W"], p["scale"], masks[:5])
+    assert_parity(sp, h, p["W"], p["scale"], masks)  # tall tiles (B > 64)
+    assert_parity(sp, h, p["W"], p["scale"], masks[:64])  # narrow tiles
+    assert_parity(sp, h, p["W"], p["scale"], masks[:5])
     # the packed copy is taken at create: later writes to W are not seen by
     # the matrix cores (W is borrowed read-only for the handle's lifetime)
     Wd.zero_()
     torch.cuda.synchronize()
-    sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_SPLIT_WORDS, 0)
     assert_parity(sp, h, p["W"], p["scale"], masks)
 
 
-def test_paths_agree_on_prefill_and_padding_junk(sp):
-    d = wl.prefill_projection(B=200)
-    masks = d["masks"].copy()
-    h, *_ = make(sp, d["W"], d["scale"])
-    outs = {}
+def test_both_paths_on_prefill_spikes_with_padding_junk(sp):
+    """Markov prefill spikes at a K that is not a multiple of 64, with every
+    padding bit of the last word set: the gather and the matrix cores each
+    match the oracle."""
+    K, N, B = 6144 - 64 * 3 + 37, 1536, 200
+    bits = wl.prefill_bits(B, K)
+    masks = wl.pack_bits(bits)
+    masks[:, -1] |= np.uint64((~((1 << (K % 64)) - 1)) & 0xFFFFFFFFFFFFFFFF)
+    rng = np.random.default_rng([42, 9, 200])
+    W = wl.uniform_weights(rng, K, N)
+    scale = wl.uniform_scales(rng, N)
+    h, *_ = make(sp, W, scale)
     for path in (sp.SPIKE_PATH_GATHER, sp.SPIKE_PATH_MFMA):
         sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, path)
-        outs[path] = bits32(gpu_forward(sp, h, masks))
-    np.testing.assert_array_equal(outs[sp.SPIKE_PATH_GATHER], outs[sp.SPIKE_PATH_MFMA])
-
-
-@pytest.mark.parametrize("waves", [4, 8])
-@pytest.mark.parametrize("depth", [1, 2, 4])
-def test_matrix_core_waves_and_depth(sp, waves, depth):
-    p = wl.small_problem(6144 - 64 * 3 + 5, 1536, 60, 0.12, seed=waves * depth)
-    h, *_ = make(sp, p["W"], p["scale"])
-    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
-    sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_WAVES, waves)
-    sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_DEPTH, depth)
-    for wps in (0, 12, 13, 40, 94):
-        sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_SPLIT_WORDS, wps)
-        assert_parity(sp, h, p["W"], p["scale"], p["masks"])
-
-
-def test_matrix_core_split_limits(sp):
-    """A K-split is refused (not run) when it needs more partial tiles than
-    the handle holds or more than one row tile."""
-    p = wl.small_problem(6144, 128, 100, 0.1, seed=3)
-    h, *_ = make(sp, p["W"], p["scale"])
-    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
-    out = torch.empty((100, 128), device="cuda")
-    for B, wps in ((100, 12), (10, 1)):  # two row tiles / 96 splits
-        sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_SPLIT_WORDS, wps)
-        with pytest.raises(sp.SpikeError) as e:
-            sp.spike_proj_forward(h, dmask(p["masks"][:B]), B, out)
-        assert e.value.code == sp.SPIKE_EUNSUPPORTED
-    sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_SPLIT_WORDS, 0)
-    assert_parity(sp, h, p["W"], p["scale"], p["masks"])
+        assert_parity(sp, h, W, scale, masks)
