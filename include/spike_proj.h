@@ -103,6 +103,27 @@ int spike_proj_forward(spike_proj_t h, const uint64_t *spike_bitmask, int32_t B,
 int spike_proj_forward_acc(spike_proj_t h, const uint64_t *spike_bitmask, int32_t B, int32_t *acc_i32,
                            void *stream);
 
+/* Handle-free variant of spike_proj_forward for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  W and scale are the device arrays that
+ * spike_proj_create takes (same layout, borrowed for the call); the result is
+ * bit-identical to spike_proj_forward on a handle over them.  The call is
+ * served by the active-column gather.  Where that gather splits K across
+ * workgroups, its INT32 partial sums and completion counters live in one
+ * library-owned device array of SPIKE_STATIC_SCRATCH_WORDS 32-bit words per
+ * GPU (4 MiB, held until the process ends), so the call needs
+ * B * (N + ceil(N/32)) <= SPIKE_STATIC_SCRATCH_WORDS and returns SPIKE_EINVAL
+ * beyond that.  It allocates nothing (no hipMalloc, hipFree or allocating
+ * library routine).  Every call on a GPU shares that GPU's array and the
+ * kernels leave it zeroed, so calls ordered on one stream are safe but calls
+ * that overlap in time on one GPU (two streams, two host threads) race and
+ * give wrong results.  Until one call has run outside graph capture on a
+ * device, each call also enqueues one small kernel on `stream` that clears
+ * the array. */
+#define SPIKE_STATIC_SCRATCH_WORDS (1 << 20)
+int spike_proj_forward_noalloc(const int8_t *W_int8_colmajor, const float *scale_fp32, int32_t K, int32_t N,
+                               const uint64_t *spike_bitmask, int32_t B, float *out_fp32, void *stream);
+
 /* Release the workspace and the handle (waits for the device first).
  * NULL is accepted. */
 int spike_proj_destroy(spike_proj_t h);

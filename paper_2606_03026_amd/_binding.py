@@ -32,7 +32,7 @@ EXPORTED = (
     "spike_proj_destroy", "spike_proj_tune", "spike_compact", "spike_stack_forward",
     "spike_stream_create", "spike_stream_forward", "spike_stream_tune", "spike_stream_destroy",
     "spike_proj_last_error", "spike_proj_shapes", "spike_mfma_plans", "spike_proj_plan_query",
-    "spike_proj_abi_version",
+    "spike_proj_abi_version", "spike_proj_forward_noalloc",
 )
 
 if not os.path.exists(LIB):
@@ -45,6 +45,7 @@ _sig = {
     "spike_proj_reserve": [_p, _i32],
     "spike_proj_forward": [_p, _p, _i32, _p, _p],
     "spike_proj_forward_acc": [_p, _p, _i32, _p, _p],
+    "spike_proj_forward_noalloc": [_p, _p, _i32, _i32, _p, _i32, _p, _p],
     "spike_proj_destroy": [_p],
     "spike_proj_tune": [_p, _i32, _i32],
     "spike_compact": [_p, _i32, _i32, _p, _p, _p],
@@ -147,6 +148,25 @@ def spike_proj_forward_acc(h: SpikeProj, mask: torch.Tensor, B: int, acc: torch.
         raise TypeError("acc must be int32")
     _check(_lib.spike_proj_forward_acc(h.ptr, _dev_ptr(mask, "mask", B * words_per_row(h.K) * 8), int(B),
                                        _dev_ptr(acc, "acc", B * h.N * 4), _stream(stream)), "spike_proj_forward_acc")
+
+
+SPIKE_STATIC_SCRATCH_WORDS = 1 << 20
+
+
+def spike_proj_forward_noalloc(W: torch.Tensor, scale: torch.Tensor, mask: torch.Tensor, B: int, out: torch.Tensor,
+                               stream=None) -> None:
+    """Handle-free forward on the library's static scratch (no device allocation)."""
+    if W.dtype != torch.int8 or W.dim() != 2:
+        raise TypeError("W must be an int8 tensor [K, N]")
+    K, N = W.shape
+    if scale.dtype != torch.float32 or scale.shape != (N,):
+        raise TypeError(f"scale must be float32 [N={N}]")
+    if out.dtype != torch.float32:
+        raise TypeError("out must be float32")
+    _check(_lib.spike_proj_forward_noalloc(_dev_ptr(W, "W"), _dev_ptr(scale, "scale"), int(K), int(N),
+                                           _dev_ptr(mask, "mask", B * words_per_row(K) * 8), int(B),
+                                           _dev_ptr(out, "out", B * N * 4), _stream(stream)),
+           "spike_proj_forward_noalloc")
 
 
 def spike_proj_destroy(h: SpikeProj) -> None:

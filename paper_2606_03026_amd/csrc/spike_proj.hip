@@ -11,6 +11,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -427,6 +428,62 @@ int parse_shape(int value, const void* W, int64_t N, const ShapeEntry** out)
 
 }  // namespace
 
+// Device memory of spike_proj_forward_noalloc: the INT32 partial sums and
+// completion counters of a K-split gather, [B][N] words followed by
+// [B][ceil(N/32)] counters.  One copy per GPU, held until the process ends.
+// In host code `scratch` is only a symbol: its device address comes from
+// hipGetSymbolAddress (per device, see static_scratch below).
+static __device__ __align__(256) uint32_t scratch[SPIKE_STATIC_SCRATCH_WORDS];
+
+__global__ __launch_bounds__(256) void k_zero_words(uint32_t* __restrict__ p, int64_t n)
+{
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+        p[i] = 0u;
+}
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+uint32_t* g_scratch_ptr[kMaxDevices];  // device address of `scratch` per device (null: not looked up yet)
+bool g_scratch_clean[kMaxDevices];     // a clearing kernel has been enqueued outside graph capture
+
+// Device address of the current device's scratch array.  The first call on a
+// device looks it up; until one call has run outside graph capture, every
+// call also enqueues a kernel on `st` that clears the array (captured calls
+// then clear it on every replay).  After that the gather's own protocol
+// leaves the array zeroed at the end of every call.
+int static_scratch(int dev, hipStream_t st, uint32_t** out)
+{
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(SPIKE_EUNSUPPORTED, "device ordinal %d is beyond the %d devices this library tracks", dev,
+                    kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess)
+            return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        g_scratch_ptr[dev] = static_cast<uint32_t*>(p);
+    }
+    if (!g_scratch_clean[dev]) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        hipError_t e = hipStreamIsCapturing(st, &cs);
+        if (e != hipSuccess)
+            return hip_fail(e, "hipStreamIsCapturing");
+        hipLaunchKernelGGL(k_zero_words, dim3(256), dim3(256), 0, st, g_scratch_ptr[dev],
+                           (int64_t)SPIKE_STATIC_SCRATCH_WORDS);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return hip_fail(e, "scratch clearing launch");
+        if (cs == hipStreamCaptureStatusNone)
+            g_scratch_clean[dev] = true;
+    }
+    *out = g_scratch_ptr[dev];
+    return SPIKE_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 int spike_proj_create(const int8_t* W, const float* scale, int32_t K, int32_t N, spike_proj_t* out_handle)
@@ -504,6 +561,52 @@ int spike_proj_forward(spike_proj_t h, const uint64_t* mask, int32_t B, float* o
 int spike_proj_forward_acc(spike_proj_t h, const uint64_t* mask, int32_t B, int32_t* acc, void* stream)
 {
     return forward_impl<true>(h, mask, B, nullptr, acc, stream);
+}
+
+int spike_proj_forward_noalloc(const int8_t* W, const float* scale, int32_t K, int32_t N, const uint64_t* mask,
+                               int32_t B, float* out, void* stream)
+{
+    g_last_error.clear();
+    if (K < 1 || K > SPIKE_MAX_K)
+        return fail(SPIKE_EINVAL, "K = %d outside [1, %d]", K, SPIKE_MAX_K);
+    if (N < 1 || N > SPIKE_MAX_N)
+        return fail(SPIKE_EINVAL, "N = %d outside [1, %d]", N, SPIKE_MAX_N);
+    if (B < 0)
+        return fail(SPIKE_EINVAL, "B = %d < 0", B);
+    const int64_t stride = (N + kMinTile - 1) / kMinTile;
+    const int64_t words = (int64_t)B * ((int64_t)N + stride);
+    if (words > SPIKE_STATIC_SCRATCH_WORDS)
+        return fail(SPIKE_EINVAL,
+                    "B * (N + ceil(N/32)) = %lld words exceeds the %d-word static scratch (B = %d, N = %d)",
+                    (long long)words, SPIKE_STATIC_SCRATCH_WORDS, B, N);
+    if (B == 0)
+        return SPIKE_OK;
+    if (!W || !scale || !mask || !out)
+        return fail(SPIKE_EINVAL, "null weight, scale, mask or output pointer");
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipGetDevice");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    uint32_t* ws = nullptr;
+    if (int rc = static_scratch(dev, st, &ws))
+        return rc;
+    // A handle on the stack over the borrowed operands and the static
+    // scratch: the gather's planner and kernels are those of spike_proj_forward.
+    spike_proj h;
+    h.W = W;
+    h.scale = scale;
+    h.K = K;
+    h.N = N;
+    h.wpr = (int32_t)words_per_row(K);
+    h.device = dev;
+    h.max_B = B;
+    h.ws = reinterpret_cast<int32_t*>(ws);
+    h.counters = ws + (int64_t)B * N;
+    h.counter_stride = (int32_t)stride;
+    h.path = SPIKE_PATH_GATHER;
+    h.shape = default_shape(W, N, 0);
+    return launch_gather<false>(&h, mask, B, out, nullptr, st);
 }
 
 int spike_proj_destroy(spike_proj_t h)
