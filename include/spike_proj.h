@@ -145,8 +145,10 @@ int spike_proj_destroy(spike_proj_t h);
  *                           the shapes the library instantiates are accepted.
  *   SPIKE_TUNE_TILES_PER_UNIT  output-channel tiles handled by one workgroup
  *                           (1..4096); the active list is built once per unit
- *   SPIKE_TUNE_XCD_SPREAD   streams only: 1 = plain unit order; 8 = keep the
- *                           tiles of one (token, projection) on one XCD
+ *   SPIKE_TUNE_XCD_SPREAD   streams only: 1 = plain unit order; 8 (default) =
+ *                           XCD x (workgroups b with b % 8 == x) runs the
+ *                           x-th contiguous eighth of the units, so every
+ *                           XCD gets the same mix of projections
  *   SPIKE_TUNE_MFMA_WAVES   waves per workgroup of the matrix-core path, which
  *                           share one tile's K range: 0 = automatic, 4, 8, 16
  *   SPIKE_TUNE_MFMA_DEPTH   k-steps of weights in flight per wave of the

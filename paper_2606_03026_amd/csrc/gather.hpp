@@ -8,14 +8,17 @@
 // One workgroup ("unit") owns a range of output-channel tiles and a slice of
 // the K axis for one spike row:
 //   1. compaction: the slice's mask words become an ascending list of active
-//      column indices in LDS (popcount + wavefront prefix scan, then each
-//      wave scatters the set bits of one word with mbcnt);
+//      column indices in LDS (popcount + wavefront prefix scan, then every
+//      thread writes the set bits of its own words at its prefix offset);
 //   2. gather: lane groups walk the list; every lane streams V bytes of each
-//      active column (one coalesced global load per column) and adds the
-//      sign-extended bytes into V INT32 registers (one VALU op per byte).
-//      Loads are software-pipelined: the next U columns are in flight while
-//      the current U are added;
-//   3. the lane groups' partial sums are added in LDS;
+//      active column (one coalesced load per column) and adds the
+//      sign-extended bytes into V INT32 registers.  Each lane keeps a ring of
+//      U load slots: a slot is added and at once refilled with the column U
+//      steps ahead, so U columns stay in flight; loads are unconditional
+//      buffer loads, and positions past the list read as zero (out-of-range
+//      offset), so no register copies or branches stall the ring;
+//   3. the lane groups of a wave are summed with cross-lane shuffles, the
+//      waves' partial sums in LDS;
 //   4. a single-slice unit converts and scales directly; with several
 //      K-slices, partials are folded into an INT32 workspace with device-
 //      scope atomic adds (exact, so order-independent), and the last unit of
@@ -36,39 +39,58 @@ template <int BLOCK>
 struct SliceLds {
     static_assert(BLOCK % 64 == 0 && BLOCK >= 64 && BLOCK <= 1024, "block must be whole waves");
     static constexpr int kWaves = BLOCK / 64;
-    uint64_t words[kMaxSliceWords];
-    int32_t offset[kMaxSliceWords];
     int32_t wave_total[kWaves];
     int32_t is_last;
 };
 
-// Active positions of mask words [w0, w0 + nw) of one row, ascending.  Bits at
-// or above K are dropped.  emit(pos, k_rel) is called once per active bit with
-// its rank pos in the list and its index k_rel relative to bit 64*w0.
-// Returns |A| of the slice in every thread.  Requires nw <= kMaxSliceWords.
+// Mask words of one thread: words [w0 + t * per, w0 + t * per + per) of the
+// slice [w0, w0 + nw), per = ceil(nw / BLOCK) <= kPer, with the bits at or
+// above K cleared (padding).  Words past the slice are zero.
+template <int BLOCK>
+struct ThreadWords {
+    static constexpr int kPer = (kMaxSliceWords + BLOCK - 1) / BLOCK;
+    uint64_t w[kPer];
+};
+
+template <int BLOCK>
+__device__ inline void load_words(const uint64_t* __restrict__ row, int w0, int nw, int K, ThreadWords<BLOCK>& tw)
+{
+    const int per = (nw + BLOCK - 1) / BLOCK;
+    const int first = threadIdx.x * per;
+#pragma unroll
+    for (int i = 0; i < ThreadWords<BLOCK>::kPer; ++i) {
+        const int j = first + i;
+        uint64_t word = 0;
+        if (i < per && j < nw) {
+            const int w = w0 + j;
+            word = row[w];
+            const int valid = K - 64 * w;  // bits of this word below K
+            if (valid < 64)
+                word &= valid <= 0 ? 0ull : ((1ull << valid) - 1ull);
+        }
+        tw.w[i] = word;
+    }
+}
+
+// Active positions of the slice whose words the threads hold, ascending:
+// emit(pos, k_rel) is called once per active bit with its rank pos in the
+// list and its index k_rel relative to bit 64*w0.  Returns |A| of the slice
+// in every thread.  Each thread owns a contiguous run of words, so the scan
+// over threads is a scan in word order; every thread emits the set bits of
+// its own words.  Two workgroup barriers.
 template <int BLOCK, class Emit>
-__device__ inline int compact_slice(const uint64_t* __restrict__ row, int w0, int nw, int K, SliceLds<BLOCK>& s,
-                                    Emit emit)
+__device__ inline int compact_words(const ThreadWords<BLOCK>& tw, int nw, SliceLds<BLOCK>& s, Emit emit)
 {
     constexpr int kWaves = SliceLds<BLOCK>::kWaves;
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int wave = t >> 6;
-    // each thread owns a contiguous run of words (one word when BLOCK >= nw),
-    // so the scan over threads is a scan in word order
     const int per = (nw + BLOCK - 1) / BLOCK;
     const int first = t * per;
-    const int last = min(first + per, nw);
     int pc = 0;
-    for (int i = first; i < last; ++i) {
-        const int w = w0 + i;
-        uint64_t word = row[w];
-        const int valid = K - 64 * w;  // bits of this word below K
-        if (valid < 64)
-            word &= valid <= 0 ? 0ull : ((1ull << valid) - 1ull);
-        s.words[i] = word;
-        pc += __popcll(word);
-    }
+#pragma unroll
+    for (int i = 0; i < ThreadWords<BLOCK>::kPer; ++i)
+        pc += __popcll(tw.w[i]);
     int incl = pc;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
@@ -86,22 +108,29 @@ __device__ inline int compact_slice(const uint64_t* __restrict__ row, int w0, in
         before += v < wave ? wt : 0;
         total += wt;
     }
-    int off = before + incl - pc;  // exclusive prefix of this thread's words
-    for (int i = first; i < last; ++i) {
-        s.offset[i] = off;
-        off += __popcll(s.words[i]);
-    }
-    __syncthreads();
-    for (int w = wave; w < nw; w += kWaves) {
-        const uint64_t wd = s.words[w];
-        if (wd == 0)
-            continue;
-        const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(wd >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)wd, 0));
-        if ((wd >> lane) & 1ull)
-            emit(s.offset[w] + below, 64 * w + lane);
+    int pos = before + incl - pc;  // exclusive prefix of this thread's words
+#pragma unroll
+    for (int i = 0; i < ThreadWords<BLOCK>::kPer; ++i) {
+        uint64_t word = tw.w[i];
+        const int kb = 64 * (first + i);
+        while (word) {
+            emit(pos++, kb + (int)__builtin_ctzll(word));
+            word &= word - 1ull;
+        }
     }
     __syncthreads();
     return total;
+}
+
+// Active positions of mask words [w0, w0 + nw) of one row (load_words, then
+// compact_words).  Requires nw <= kMaxSliceWords.
+template <int BLOCK, class Emit>
+__device__ inline int compact_slice(const uint64_t* __restrict__ row, int w0, int nw, int K, SliceLds<BLOCK>& s,
+                                    Emit emit)
+{
+    ThreadWords<BLOCK> tw;
+    load_words<BLOCK>(row, w0, nw, K, tw);
+    return compact_words<BLOCK>(tw, nw, s, emit);
 }
 
 // Cross-workgroup hand-off without cache maintenance.  A device-scope
@@ -133,12 +162,19 @@ __device__ inline T load_hint(const T* p)
 template <int V, bool NT>
 struct Chunk;
 
+// acc[i] += sign-extended byte i of d: one VALU op per byte, an SDWA add
+// whose first operand selects and sign-extends the byte (the compiler's own
+// lowering takes a bit-field extract per byte plus three-operand adds).
 __device__ inline void add_i8x4(int32_t* acc, uint32_t d)
 {
-    acc[0] += (int32_t)(int8_t)(d & 0xffu);
-    acc[1] += (int32_t)(int8_t)((d >> 8) & 0xffu);
-    acc[2] += (int32_t)(int8_t)((d >> 16) & 0xffu);
-    acc[3] += ((int32_t)d) >> 24;
+    asm("v_add_u32_sdwa %0, sext(%1), %0 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_0 src1_sel:DWORD"
+        : "+v"(acc[0]) : "v"(d));
+    asm("v_add_u32_sdwa %0, sext(%1), %0 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1 src1_sel:DWORD"
+        : "+v"(acc[1]) : "v"(d));
+    asm("v_add_u32_sdwa %0, sext(%1), %0 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_2 src1_sel:DWORD"
+        : "+v"(acc[2]) : "v"(d));
+    asm("v_add_u32_sdwa %0, sext(%1), %0 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3 src1_sel:DWORD"
+        : "+v"(acc[3]) : "v"(d));
 }
 
 template <bool NT>
@@ -180,6 +216,56 @@ struct Chunk<1, NT> {  // any N, any alignment
     __device__ void add(int32_t* acc) const { acc[0] += (int32_t)v; }
 };
 
+// The same loads through a buffer resource (base and size in scalar
+// registers, a 32-bit byte offset per lane): no 64-bit address arithmetic,
+// and an offset at or past the resource's size reads as zero without a
+// memory access.  NT sets the nontemporal cache policy.
+constexpr uint32_t kOutOfRange = 0x80000000u;  // offset that is always past the resource
+constexpr int64_t kBufMaxBytes = 0x7fffff00;   // largest weight matrix the buffer path addresses
+constexpr int kBufferFlags = 0x00020000;       // buffer resource word 3: 32-bit data format (gfx9)
+
+__device__ inline __amdgpu_buffer_rsrc_t weight_resource(const int8_t* base, int64_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(base), 0, (int)bytes, kBufferFlags);
+}
+
+template <int V, bool NT>
+struct BufChunk;
+template <bool NT>
+struct BufChunk<16, NT> {
+    u32x4 v;
+    __device__ void load(__amdgpu_buffer_rsrc_t r, uint32_t off) { v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, NT ? 2 : 0); }
+    __device__ void add(int32_t* acc) const
+    {
+        add_i8x4(acc + 0, v.x);
+        add_i8x4(acc + 4, v.y);
+        add_i8x4(acc + 8, v.z);
+        add_i8x4(acc + 12, v.w);
+    }
+};
+template <bool NT>
+struct BufChunk<8, NT> {
+    u32x2 v;
+    __device__ void load(__amdgpu_buffer_rsrc_t r, uint32_t off) { v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, NT ? 2 : 0); }
+    __device__ void add(int32_t* acc) const
+    {
+        add_i8x4(acc + 0, v.x);
+        add_i8x4(acc + 4, v.y);
+    }
+};
+template <bool NT>
+struct BufChunk<4, NT> {
+    uint32_t v;
+    __device__ void load(__amdgpu_buffer_rsrc_t r, uint32_t off) { v = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, NT ? 2 : 0); }
+    __device__ void add(int32_t* acc) const { add_i8x4(acc, v); }
+};
+template <bool NT>
+struct BufChunk<1, NT> {
+    uint8_t v;
+    __device__ void load(__amdgpu_buffer_rsrc_t r, uint32_t off) { v = __builtin_amdgcn_raw_buffer_load_b8(r, off, 0, NT ? 2 : 0); }
+    __device__ void add(int32_t* acc) const { acc[0] += (int32_t)(int8_t)v; }
+};
+
 // Launch shape.  Lane groups of LG lanes (a group may span waves); a lane
 // covers V consecutive output channels, a group one tile of TB = LG * V
 // channels of one column at a time; U columns per group are in flight;
@@ -190,7 +276,7 @@ struct Shape {
     static constexpr bool NT = NT_;
     static constexpr int kTile = V * LG;
     static constexpr int kGroups = BLOCK / LG;
-    static_assert(BLOCK % LG == 0 && LG >= 1 && LG <= BLOCK, "lane groups must tile the workgroup");
+    static_assert(BLOCK % LG == 0 && LG >= 1 && LG <= 64 && 64 % LG == 0, "lane groups must tile a wave");
     static_assert(U >= 1 && U <= 16, "unroll");
 };
 
@@ -242,6 +328,72 @@ __device__ inline void gather_columns(const int8_t* __restrict__ W, int64_t N, i
         cur[u].add(acc);
 }
 
+// gather_columns on a buffer resource over the slice's columns (offset 0 =
+// column kbase), as a ring of U load slots per lane.  Round r of group g
+// takes the U consecutive list positions r * U * G + g * U + [0, U), read
+// from LDS as U/2 32-bit words.  The lane groups of a wave run the same
+// number of rounds (that of the wave's first group, which has the most
+// positions); positions past the list load zeros.  The list must hold U * G
+// readable entries past its end (list_lds reserves them).
+template <class S>
+__device__ inline void gather_ring(__amdgpu_buffer_rsrc_t w, uint32_t N, uint32_t n_lane, bool lane_in_range,
+                                   const uint16_t* list, int cnt, int32_t (&acc)[S::V])
+{
+    constexpr int G = S::kGroups;
+    constexpr int U = S::U;
+    constexpr int STEP = U * G;
+    static_assert(U % 2 == 0, "list entries are read in pairs");
+#pragma unroll
+    for (int j = 0; j < S::V; ++j)
+        acc[j] = 0;
+    const int g = threadIdx.x / S::LG;
+    const int g_first = __builtin_amdgcn_readfirstlane(g);
+    const int rounds = cnt > g_first * U ? (cnt - g_first * U + STEP - 1) / STEP : 0;
+    const uint32_t* pairs = reinterpret_cast<const uint32_t*>(list + g * U);
+    // byte offsets of round r's columns in this lane's run; positions past
+    // the list get an offset past the resource.  (Masks, not selects: a
+    // select of a loaded value would be turned into a branch around the load.)
+    auto offsets = [&](int r, uint32_t (&off)[U]) {
+        uint32_t two[U / 2];
+#pragma unroll
+        for (int i = 0; i < U / 2; ++i)
+            two[i] = pairs[r * (STEP / 2) + i];
+        const int p0 = r * STEP + g * U;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t col = u % 2 ? two[u / 2] >> 16 : two[u / 2] & 0xffffu;
+            const uint32_t keep = (p0 + u < cnt && lane_in_range) ? ~0u : 0u;
+            off[u] = ((__umul24(col, N) + n_lane) & keep) | (kOutOfRange & ~keep);  // col * N < 2^31
+        }
+    };
+    BufChunk<S::V, S::NT> slot[U];
+    {
+        uint32_t off[U];
+        offsets(0, off);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            slot[u].load(w, off[u]);
+    }
+    // The scheduling barriers keep every slot's refill after its add, so a
+    // slot's old and new values never live at once (no register copies) and
+    // U loads stay in flight; the round's list entries are read first.
+    for (int r = 1; r < rounds; ++r) {
+        uint32_t off[U];
+        offsets(r, off);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            slot[u].add(acc);
+            slot[u].load(w, off[u]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    if (rounds > 0) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            slot[u].add(acc);
+    }
+}
+
 // Output of one unit: either FP32 y (ACC == false) or the raw INT32 sums.
 template <bool ACC>
 __device__ inline void store_result(float* out_row, int32_t* acc_row, const float* __restrict__ scale, int64_t n,
@@ -255,18 +407,66 @@ __device__ inline void store_result(float* out_row, int32_t* acc_row, const floa
     }
 }
 
+// The outputs of one tile: the waves' partial sums (red[q * TB + e] for
+// wave q and channel n_tile0 + e) are added and written, as FP32 y or raw
+// INT32 sums.  Where N, the output row and the scales allow it, each thread
+// handles four channels with 16-byte LDS reads, scale loads and nontemporal
+// stores: a tile then costs two store instructions instead of eight, and
+// narrow stores stall the in-order vector memory pipeline of the CU (every
+// weight load queued behind a store waits with it).
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <class S, bool ACC>
+__device__ inline void finish_tile(const int32_t* red, int64_t n_tile0, int N, const float* __restrict__ scale,
+                                   float* out_row, int32_t* acc_row)
+{
+    constexpr int TB = S::kTile;
+    constexpr int kWaves = S::BLOCK / 64;
+    const uintptr_t dst = ACC ? reinterpret_cast<uintptr_t>(acc_row) : reinterpret_cast<uintptr_t>(out_row);
+    const uintptr_t sc = ACC ? 0 : reinterpret_cast<uintptr_t>(scale);
+    if (TB % 4 == 0 && N % 4 == 0 && ((dst | sc) & 15) == 0) {
+        for (int e = 4 * (int)threadIdx.x; e < TB && n_tile0 + e < N; e += 4 * S::BLOCK) {
+            i32x4 sum = *reinterpret_cast<const i32x4*>(red + e);
+#pragma unroll
+            for (int q = 1; q < kWaves; ++q)
+                sum += *reinterpret_cast<const i32x4*>(red + q * TB + e);
+            if constexpr (ACC) {
+                __builtin_nontemporal_store(sum, reinterpret_cast<i32x4*>(acc_row + n_tile0 + e));
+            } else {
+                const f32x4 s4 = *reinterpret_cast<const f32x4*>(scale + n_tile0 + e);
+                f32x4 y;
+                y.x = (float)sum.x * s4.x;  // per channel: one exact-or-RNE conversion, one binary32 multiply
+                y.y = (float)sum.y * s4.y;
+                y.z = (float)sum.z * s4.z;
+                y.w = (float)sum.w * s4.w;
+                __builtin_nontemporal_store(y, reinterpret_cast<f32x4*>(out_row + n_tile0 + e));
+            }
+        }
+        return;
+    }
+    for (int e = threadIdx.x; e < TB && n_tile0 + e < N; e += S::BLOCK) {
+        int32_t sum = 0;
+#pragma unroll
+        for (int q = 0; q < kWaves; ++q)
+            sum += red[q * TB + e];
+        store_result<ACC>(out_row, acc_row, scale, n_tile0 + e, sum);
+    }
+}
+
 // Dynamic LDS of a unit: the active list (uint16 per bit of the slice) and
-// the partial sums of every lane group.  With one tile per unit the two
-// share the same bytes (the list is dead before the reduction).
+// the partial sums of every wave.  With one tile per unit the two share the
+// same bytes (the list is dead before the reduction).
 template <class S>
 constexpr size_t list_lds(int slice_words)
 {
-    return ((size_t)slice_words * 64 * sizeof(uint16_t) + 15) / 16 * 16;
+    // every bit of the slice, plus one round of the ring gather past the end
+    return (((size_t)slice_words * 64 + S::U * S::kGroups) * sizeof(uint16_t) + 15) / 16 * 16;
 }
 template <class S>
 constexpr size_t red_lds()
 {
-    return (size_t)S::BLOCK * S::V * sizeof(int32_t);
+    return (size_t)(S::BLOCK / 64) * S::kTile * sizeof(int32_t);
 }
 template <class S>
 constexpr size_t unit_dyn_lds(int slice_words, int tiles_per_unit)
@@ -275,14 +475,12 @@ constexpr size_t unit_dyn_lds(int slice_words, int tiles_per_unit)
     return tiles_per_unit == 1 ? (l > r ? l : r) : l + r;
 }
 
-// Descriptor of one projection in a multi-projection stream.
-struct StreamDesc {
+// Weight and scale pointers of one (weight set, projection) of a
+// multi-projection stream: the stream's device operand table holds one per
+// handle, set-major.
+struct StreamOperands {
     const int8_t* W;
     const float* scale;
-    int32_t K;
-    int32_t wpr;
-    int64_t mask_off;  // word offset of this projection's row within a token
-    int64_t out_off;   // float offset of this projection's output within a token
 };
 
 // Per-projection layout of a token, passed by value as a kernel argument so
@@ -306,45 +504,56 @@ struct DirectOperands {
     __device__ const float* scales() const { return scale; }
 };
 __device__ inline DirectOperands operands_of(const DirectOperands& d) { return d; }
-__device__ inline DirectOperands operands_of(const StreamDesc* d) { return DirectOperands{d->W, d->scale}; }
+__device__ inline DirectOperands operands_of(const StreamOperands* d) { return DirectOperands{d->W, d->scale}; }
 
 // One unit: K-slice [w0, w0 + nw) of one row, tiles [tile0, tile0 + n_tiles_here).
-template <class S, bool ACC, class Src>
+// BUF: weight loads through a buffer resource (needs K * N <= kBufMaxBytes).
+template <class S, bool ACC, bool BUF, class Src>
 __device__ inline void run_unit(const Src& src, int K, int N, const uint64_t* __restrict__ row, int w0, int nw,
                                 int tile0, int n_tiles_here, int n_slices, int32_t* ws_row, uint32_t* counters_row,
                                 float* out_row, int32_t* acc_row, SliceLds<S::BLOCK>& s, uint8_t* dyn)
 {
     constexpr int TB = S::kTile;
-    constexpr int G = S::kGroups;
+    constexpr int kWaves = S::BLOCK / 64;
     uint16_t* list = reinterpret_cast<uint16_t*>(dyn);
-    const int cnt = compact_slice<S::BLOCK>(row, w0, nw, K, s, [&](int pos, int k) { list[pos] = (uint16_t)k; });
+    ThreadWords<S::BLOCK> tw;
+    load_words<S::BLOCK>(row, w0, nw, K, tw);
     const DirectOperands ops = operands_of(src);
     const int8_t* __restrict__ W = ops.weights();
     const float* __restrict__ scale = ops.scales();
+    const int cnt = compact_words<S::BLOCK>(tw, nw, s, [&](int pos, int k) { list[pos] = (uint16_t)k; });
     int32_t* red = reinterpret_cast<int32_t*>(n_tiles_here == 1 ? dyn : dyn + list_lds<S>(nw));
 
     const int lg = threadIdx.x % S::LG;
-    const int g = threadIdx.x / S::LG;
+    const int lane = threadIdx.x % 64;
+    const int wave = threadIdx.x / 64;
+    // the slice's columns [64 w0, K) as a buffer resource (unused without BUF)
+    const __amdgpu_buffer_rsrc_t wres = weight_resource(W + 64ll * w0 * N, BUF ? (int64_t)(K - 64 * w0) * N : 0);
     for (int tt = 0; tt < n_tiles_here; ++tt) {
         const int tile = tile0 + tt;
         const int64_t n_tile0 = (int64_t)tile * TB;
         const int64_t n_lane = n_tile0 + (int64_t)lg * S::V;
         int32_t acc[S::V];
-        gather_columns<S>(W, N, 64ll * w0, n_lane, n_lane < N, list, cnt, acc);
-        __syncthreads();  // list dead (one tile) / previous tile's reduction read
+        if constexpr (BUF)
+            gather_ring<S>(wres, (uint32_t)N, (uint32_t)n_lane, n_lane < N, list, cnt, acc);
+        else
+            gather_columns<S>(W, N, 64ll * w0, n_lane, n_lane < N, list, cnt, acc);
+        // the lane groups of a wave are folded into its first group
 #pragma unroll
-        for (int j = 0; j < S::V; ++j)
-            red[g * TB + lg * S::V + j] = acc[j];
+        for (int d = S::LG; d < 64; d <<= 1)
+#pragma unroll
+            for (int j = 0; j < S::V; ++j)
+                acc[j] += __shfl_xor(acc[j], d, 64);
+        __syncthreads();  // list dead (one tile) / previous tile's reduction read
+        if (lane < S::LG) {
+#pragma unroll
+            for (int j = 0; j < S::V; ++j)
+                red[wave * TB + lg * S::V + j] = acc[j];
+        }
         __syncthreads();
 
         if (n_slices == 1) {
-            for (int e = threadIdx.x; e < TB && n_tile0 + e < N; e += S::BLOCK) {
-                int32_t sum = 0;
-#pragma unroll
-                for (int q = 0; q < G; ++q)
-                    sum += red[q * TB + e];
-                store_result<ACC>(out_row, acc_row, scale, n_tile0 + e, sum);
-            }
+            finish_tile<S, ACC>(red, n_tile0, N, scale, out_row, acc_row);
             continue;
         }
 
@@ -353,7 +562,7 @@ __device__ inline void run_unit(const Src& src, int K, int N, const uint64_t* __
             for (int e = threadIdx.x; e < TB && n_tile0 + e < N; e += S::BLOCK) {
                 int32_t sum = 0;
 #pragma unroll
-                for (int q = 0; q < G; ++q)
+                for (int q = 0; q < kWaves; ++q)
                     sum += red[q * TB + e];
                 atomicAdd(ws_row + n_tile0 + e, sum);
             }
@@ -377,7 +586,7 @@ __device__ inline void run_unit(const Src& src, int K, int N, const uint64_t* __
 // One launch of B spike rows against one weight matrix: unit id ->
 // (row b, tile group, slice), slices fastest.  A unit covers tiles_per_unit
 // consecutive tiles (the last group may hold fewer).
-template <class S, bool ACC>
+template <class S, bool ACC, bool BUF>
 __global__ __launch_bounds__(S::BLOCK) __attribute__((amdgpu_waves_per_eu(4))) void k_gather(const int8_t* __restrict__ W, const float* __restrict__ scale,
                                                      int K, int N, const uint64_t* __restrict__ mask, int wpr,
                                                      int slice_words, int n_slices, int n_tiles, int tiles_per_unit,
@@ -397,43 +606,46 @@ __global__ __launch_bounds__(S::BLOCK) __attribute__((amdgpu_waves_per_eu(4))) v
     const int tile0 = tg * tiles_per_unit;
     const int nt = min(tiles_per_unit, n_tiles - tile0);
     const int64_t rowN = (int64_t)b * N;
-    run_unit<S, ACC>(DirectOperands{W, scale}, K, N, mask + (int64_t)b * wpr, w0, nw, tile0, nt, n_slices,
+    run_unit<S, ACC, BUF>(DirectOperands{W, scale}, K, N, mask + (int64_t)b * wpr, w0, nw, tile0, nt, n_slices,
                      n_slices > 1 ? ws + rowN : nullptr,
                      n_slices > 1 ? counters + (int64_t)b * counter_stride : nullptr, ACC ? nullptr : out + rowN,
                      ACC ? acc_out + rowN : nullptr, s, dyn);
 }
 
-template <class S>
+template <class S, bool BUF>
 __global__ __launch_bounds__(S::BLOCK) __attribute__((amdgpu_waves_per_eu(4))) void k_stream(
-    const StreamDesc* __restrict__ desc, const StreamLayout layout, int n_proj, int n_sets, int N, int n_tiles,
+    const StreamOperands* __restrict__ desc, const StreamLayout layout, int n_proj, int n_sets, int N, int n_tiles,
     int tiles_per_unit, int n_items, int xcd_spread, const uint64_t* __restrict__ masks, int64_t mask_stride,
     float* out, int64_t out_stride)
 {
     __shared__ SliceLds<S::BLOCK> s;
     extern __shared__ __align__(16) uint8_t dyn[];
     const int n_groups = (n_tiles + tiles_per_unit - 1) / tiles_per_unit;
-    int tg, item;
+    const int n_units = n_items * n_groups;
+    int unit = blockIdx.x;
     if (xcd_spread > 1) {
-        // Workgroups are dispatched round-robin over the XCDs; keep the tile
-        // groups of one (token, projection) item on the same XCD.
-        const int per = xcd_spread * n_groups;
-        const int p = blockIdx.x % per;
-        item = (blockIdx.x / per) * xcd_spread + p % xcd_spread;
-        tg = p / xcd_spread;
-        if (item >= n_items)
+        // Workgroups are dispatched to the XCDs round-robin (block b to XCD
+        // b % xcd_spread, in order).  XCD x runs the contiguous unit range
+        // [x * per, (x + 1) * per): every XCD then gets the same mix of
+        // projections (TCAM and down items differ 4x in work; plain order
+        // gives some XCDs twice the down tiles of others), and the tiles of
+        // one item run back to back on one XCD, whose L2 keeps their spike
+        // words.
+        const int per = (n_units + xcd_spread - 1) / xcd_spread;
+        unit = (blockIdx.x % xcd_spread) * per + blockIdx.x / xcd_spread;
+        if (unit >= n_units)
             return;
-    } else {
-        tg = blockIdx.x % n_groups;
-        item = blockIdx.x / n_groups;
     }
+    const int tg = unit % n_groups;
+    const int item = unit / n_groups;
     const int t = item / n_proj;
     const int j = item - t * n_proj;
     const int K = layout.K[j];
     const uint64_t* row = masks + (int64_t)t * mask_stride + layout.mask_off[j];
-    const StreamDesc* d = desc + (t % n_sets) * n_proj + j;  // read after the spike words are requested
+    const StreamOperands* d = desc + (t % n_sets) * n_proj + j;  // read after the spike words are requested
     const int tile0 = tg * tiles_per_unit;
     const int nt = min(tiles_per_unit, n_tiles - tile0);
-    run_unit<S, false>(d, K, N, row, 0, (K + 63) / 64, tile0, nt, 1, nullptr, nullptr,
+    run_unit<S, false, BUF>(d, K, N, row, 0, (K + 63) / 64, tile0, nt, 1, nullptr, nullptr,
                        out + (int64_t)t * out_stride + (int64_t)j * N, nullptr, s, dyn);
 }
 

@@ -50,18 +50,21 @@ using GatherFn = void (*)(const spike_proj*, const uint64_t*, int32_t, int, int,
                           hipStream_t);
 using StreamFn = void (*)(const spike_stream*, int, unsigned, const uint64_t*, float*, hipStream_t);
 
+// Kernels of a shape come in two variants: weight loads through a buffer
+// resource (index 1, matrices of at most spk::kBufMaxBytes) and through
+// 64-bit addresses (index 0, any size).
 struct ShapeEntry {
     int code;
     int vec, lanes, unroll, block;
-    GatherFn gather;
-    GatherFn gather_acc;
-    StreamFn stream;
+    GatherFn gather[2];
+    GatherFn gather_acc[2];
+    StreamFn stream[2];
 };
 
-template <class S, bool ACC>
+template <class S, bool ACC, bool BUF>
 void launch_gather_t(const spike_proj* h, const uint64_t* mask, int32_t B, int sw, int n_slices, int n_tiles,
                      int tpu, float* out, int32_t* acc, hipStream_t st);
-template <class S>
+template <class S, bool BUF>
 void launch_stream_t(const spike_stream* s, int n_tiles, unsigned units, const uint64_t* masks, float* out,
                      hipStream_t st);
 
@@ -69,26 +72,31 @@ template <int V, int LG, int U, int BLOCK, bool NT = false>
 constexpr ShapeEntry entry()
 {
     using S = spk::Shape<V, LG, U, BLOCK, NT>;
-    return ShapeEntry{SPIKE_SHAPE(V, LG, U, BLOCK) | (NT ? SPIKE_SHAPE_NT : 0), V, LG, U, BLOCK,
-                      &launch_gather_t<S, false>, &launch_gather_t<S, true>, &launch_stream_t<S>};
+    return ShapeEntry{SPIKE_SHAPE(V, LG, U, BLOCK) | (NT ? SPIKE_SHAPE_NT : 0),
+                      V,
+                      LG,
+                      U,
+                      BLOCK,
+                      {&launch_gather_t<S, false, false>, &launch_gather_t<S, false, true>},
+                      {&launch_gather_t<S, true, false>, &launch_gather_t<S, true, true>},
+                      {&launch_stream_t<S, false>, &launch_stream_t<S, true>}};
 }
 
 const ShapeEntry kShapes[] = {
-    // half-column tiles, nontemporal weight loads (throughput: streams, batched rows)
-    entry<16, 32, 2, 256, true>(), entry<16, 32, 1, 256, true>(), entry<16, 32, 3, 256, true>(),
-    entry<16, 32, 4, 256, true>(), entry<16, 32, 2, 512, true>(), entry<16, 32, 2, 128, true>(),
-    entry<16, 64, 2, 256, true>(), entry<16, 16, 2, 256, true>(), entry<8, 64, 4, 256, true>(),
-    entry<8, 64, 2, 256, true>(), entry<8, 32, 2, 256, true>(),
+    // half-column tiles, nontemporal weight loads (throughput: streams, batched rows), ring depths
+    entry<16, 32, 4, 256, true>(), entry<16, 32, 2, 256, true>(), entry<16, 32, 6, 256, true>(),
+    entry<16, 32, 8, 256, true>(), entry<16, 32, 4, 512, true>(), entry<16, 64, 4, 256, true>(),
+    entry<8, 64, 4, 256, true>(), entry<8, 32, 4, 256, true>(),
     // the same with cached loads (weights re-read soon, e.g. warm caches)
-    entry<16, 32, 2, 256>(), entry<16, 32, 4, 256>(), entry<8, 64, 4, 256>(), entry<8, 32, 4, 256>(),
-    // full-column lane groups (measured slower; kept for comparison)
-    entry<16, 96, 2, 768>(), entry<8, 192, 4, 768>(),
+    entry<16, 32, 4, 256>(), entry<8, 64, 4, 256>(),
     // narrow tiles (decode latency)
     entry<4, 64, 4, 256>(), entry<4, 16, 8, 256>(), entry<4, 16, 4, 1024>(), entry<4, 16, 16, 256>(),
-    entry<4, 8, 8, 1024>(), entry<4, 8, 16, 512>(), entry<8, 16, 8, 1024>(),
     // any N, any alignment
     entry<1, 64, 4, 256>(),
 };
+
+// The buffer-resource kernels address the weight matrix with 32-bit offsets.
+bool fits_buffer(int64_t K, int64_t N) { return K * N <= spk::kBufMaxBytes; }
 
 const ShapeEntry* find_shape(int code)
 {
@@ -108,12 +116,11 @@ bool shape_fits(const ShapeEntry* e, const void* W, int64_t N)
 }
 
 // Default throughput shape for a vector width (0: the widest that fits):
-// 512-byte tiles with nontemporal loads measured fastest on the 1536-wide
-// decode stack (and 16-byte lanes need N to be a multiple of 512 to keep
-// every lane busy).
+// 512-byte tiles with nontemporal loads, four columns in flight per lane
+// (16-byte lanes need N to be a multiple of 512 to keep every lane busy).
 const ShapeEntry* default_shape(const void* W, int64_t N, int vec)
 {
-    static const int by_vec[][2] = {{16, SPIKE_SHAPE(16, 32, 2, 256) | SPIKE_SHAPE_NT},
+    static const int by_vec[][2] = {{16, SPIKE_SHAPE(16, 32, 4, 256) | SPIKE_SHAPE_NT},
                                     {8, SPIKE_SHAPE(8, 64, 4, 256) | SPIKE_SHAPE_NT},
                                     {4, SPIKE_SHAPE(4, 64, 4, 256)},
                                     {1, SPIKE_SHAPE(1, 64, 4, 256)}};
@@ -175,36 +182,37 @@ struct spike_stream {
     int32_t n_proj = 0, n_sets = 0, n_tokens = 0, N = 0;
     const ShapeEntry* shape = nullptr;
     int tiles_per_unit = 1;
-    int xcd_spread = 1;
+    int xcd_spread = 8;  // contiguous unit ranges per XCD (see k_stream)
     int max_wpr = 0;
     int device = 0;
     int64_t mask_stride = 0, out_stride = 0;
-    spk::StreamDesc* d_desc = nullptr;
+    bool buf = true;  // every weight matrix fits the buffer-resource kernels
+    spk::StreamOperands* d_ops = nullptr;  // device operand table [n_sets][n_proj]
     spk::StreamLayout layout{};
     std::vector<const void*> weights;  // to re-check alignment when the shape changes
 };
 
 namespace {
 
-template <class S, bool ACC>
+template <class S, bool ACC, bool BUF>
 void launch_gather_t(const spike_proj* h, const uint64_t* mask, int32_t B, int sw, int n_slices, int n_tiles,
                      int tpu, float* out, int32_t* acc, hipStream_t st)
 {
     const size_t dyn = spk::unit_dyn_lds<S>(sw, tpu);
     const int64_t groups = (n_tiles + tpu - 1) / tpu;
     const int64_t units = (int64_t)B * groups * n_slices;
-    hipLaunchKernelGGL((spk::k_gather<S, ACC>), dim3((unsigned)units), dim3(S::BLOCK), dyn, st, h->W, h->scale,
+    hipLaunchKernelGGL((spk::k_gather<S, ACC, BUF>), dim3((unsigned)units), dim3(S::BLOCK), dyn, st, h->W, h->scale,
                        h->K, h->N, mask, h->wpr, sw, n_slices, n_tiles, tpu, h->ws, h->counters, h->counter_stride,
                        out, acc);
 }
 
-template <class S>
+template <class S, bool BUF>
 void launch_stream_t(const spike_stream* s, int n_tiles, unsigned units, const uint64_t* masks, float* out,
                      hipStream_t st)
 {
     const size_t dyn = spk::unit_dyn_lds<S>(s->max_wpr, s->tiles_per_unit);
     const int n_items = s->n_tokens * s->n_proj;
-    hipLaunchKernelGGL((spk::k_stream<S>), dim3(units), dim3(S::BLOCK), dyn, st, s->d_desc, s->layout, s->n_proj,
+    hipLaunchKernelGGL((spk::k_stream<S, BUF>), dim3(units), dim3(S::BLOCK), dyn, st, s->d_ops, s->layout, s->n_proj,
                        s->n_sets, s->N, n_tiles, s->tiles_per_unit, n_items, s->xcd_spread, masks, s->mask_stride,
                        out, s->out_stride);
 }
@@ -315,7 +323,9 @@ int launch_gather(const spike_proj* h, const uint64_t* mask, int32_t B, float* o
     const int64_t units = (int64_t)B * n_groups * p.n_slices;
     if (units > 0x7fffffff)
         return fail(SPIKE_EUNSUPPORTED, "launch of %lld workgroups is too large", (long long)units);
-    (ACC ? p.shape->gather_acc : p.shape->gather)(h, mask, B, p.sw, p.n_slices, p.n_tiles, p.tpu, out, acc, st);
+    const int buf = fits_buffer(h->K, h->N) ? 1 : 0;
+    (ACC ? p.shape->gather_acc[buf] : p.shape->gather[buf])(h, mask, B, p.sw, p.n_slices, p.n_tiles, p.tpu, out, acc,
+                                                             st);
     const hipError_t e = hipGetLastError();
     return e == hipSuccess ? SPIKE_OK : hip_fail(e, "gather launch");
 }
@@ -758,6 +768,7 @@ int spike_stream_create(const spike_proj_t* projs, int32_t n_proj, int32_t n_set
         return fail(SPIKE_EINVAL, "projection 0 is null");
     const int32_t N = projs[0]->N;
     int max_wpr = 0;
+    bool buf = true;
     std::vector<const void*> weights;
     for (int64_t i = 0; i < n_handles; ++i) {
         const spike_proj* p = projs[i];
@@ -772,6 +783,7 @@ int spike_stream_create(const spike_proj_t* projs, int32_t n_proj, int32_t n_set
         if (p->wpr > spk::kMaxSliceWords)
             return fail(SPIKE_EUNSUPPORTED, "stream projections need K <= %d", 64 * spk::kMaxSliceWords);
         max_wpr = std::max(max_wpr, p->wpr);
+        buf = buf && fits_buffer(p->K, p->N);
         weights.push_back(p->W);
     }
     // the widest default shape whose loads fit every weight matrix
@@ -792,51 +804,45 @@ int spike_stream_create(const spike_proj_t* projs, int32_t n_proj, int32_t n_set
     const int64_t n_tiles = (N + tile - 1) / tile;
     if (((int64_t)n_tokens * n_proj + 8) * n_tiles > 0x7fffffff)
         return fail(SPIKE_EUNSUPPORTED, "stream of %d tokens is too large for one launch", n_tokens);
-    std::vector<spk::StreamDesc> desc((size_t)n_handles);
+    std::vector<spk::StreamOperands> ops((size_t)n_handles);
     int64_t moff = 0;
-    for (int j = 0; j < n_proj; ++j) {
-        for (int set = 0; set < n_sets; ++set) {
-            const spike_proj* p = projs[(int64_t)set * n_proj + j];
-            spk::StreamDesc& d = desc[(size_t)set * n_proj + j];
-            d.W = p->W;
-            d.scale = p->scale;
-            d.K = p->K;
-            d.wpr = p->wpr;
-            d.mask_off = moff;
-            d.out_off = (int64_t)j * N;
-        }
-        moff += projs[j]->wpr;
-    }
     spike_stream* s = new (std::nothrow) spike_stream;
     if (!s)
         return fail(SPIKE_ENOMEM, "stream allocation failed");
+    for (int j = 0; j < n_proj; ++j) {
+        for (int set = 0; set < n_sets; ++set) {
+            const spike_proj* p = projs[(int64_t)set * n_proj + j];
+            ops[(size_t)set * n_proj + j] = spk::StreamOperands{p->W, p->scale};
+        }
+        s->layout.K[j] = projs[j]->K;
+        s->layout.mask_off[j] = (int32_t)std::min<int64_t>(moff, 0x7fffffff);
+        moff += projs[j]->wpr;
+    }
+    if (moff > 0x7fffffff) {
+        delete s;
+        return fail(SPIKE_EUNSUPPORTED, "token mask stride too large");
+    }
     s->n_proj = n_proj;
     s->n_sets = n_sets;
     s->n_tokens = n_tokens;
     s->N = N;
     s->shape = shape;
     s->max_wpr = max_wpr;
+    s->buf = buf;
     s->mask_stride = moff;
     s->out_stride = (int64_t)n_proj * N;
-    for (int j = 0; j < n_proj; ++j) {
-        s->layout.K[j] = desc[j].K;
-        s->layout.mask_off[j] = (int32_t)desc[j].mask_off;
-    }
-    if (moff > 0x7fffffff) {
-        delete s;
-        return fail(SPIKE_EUNSUPPORTED, "token mask stride too large");
-    }
     s->weights = std::move(weights);
+    const size_t ops_bytes = ops.size() * sizeof(spk::StreamOperands);
     hipError_t e = hipGetDevice(&s->device);
     if (e == hipSuccess)
-        e = hipMalloc(&s->d_desc, desc.size() * sizeof(spk::StreamDesc));
+        e = hipMalloc(&s->d_ops, ops_bytes);
     if (e == hipSuccess)
-        e = hipMemcpy(s->d_desc, desc.data(), desc.size() * sizeof(spk::StreamDesc), hipMemcpyHostToDevice);
+        e = hipMemcpy(s->d_ops, ops.data(), ops_bytes, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
-        if (s->d_desc)
-            (void)hipFree(s->d_desc);
+        if (s->d_ops)
+            (void)hipFree(s->d_ops);
         delete s;
-        return hip_fail(e, "stream descriptor upload");
+        return hip_fail(e, "stream operand table upload");
     }
     *out_stream = s;
     return SPIKE_OK;
@@ -869,6 +875,7 @@ int spike_stream_tune(spike_stream_t s, int32_t key, int32_t value)
             return fail(SPIKE_EINVAL, "xcd spread must be 1 or 8, got %d", value);
         s->xcd_spread = value;
         return SPIKE_OK;
+
     default:
         return fail(SPIKE_EINVAL, "key %d does not apply to a stream", key);
     }
@@ -888,11 +895,11 @@ int spike_stream_forward(spike_stream_t s, const uint64_t* masks, float* out, vo
     const int tpu = std::min(s->tiles_per_unit, n_tiles);
     const int n_groups = (n_tiles + tpu - 1) / tpu;
     const int64_t n_items = (int64_t)s->n_tokens * s->n_proj;
-    const int64_t padded = (n_items + s->xcd_spread - 1) / s->xcd_spread * s->xcd_spread;
-    const unsigned units = (unsigned)(padded * n_groups);
+    const int64_t n_units = n_items * n_groups;
+    const unsigned units = (unsigned)((n_units + s->xcd_spread - 1) / s->xcd_spread * s->xcd_spread);
     const int saved = s->tiles_per_unit;
     s->tiles_per_unit = tpu;  // launch with the clamped value
-    s->shape->stream(s, n_tiles, units, masks, out, static_cast<hipStream_t>(stream));
+    s->shape->stream[s->buf ? 1 : 0](s, n_tiles, units, masks, out, static_cast<hipStream_t>(stream));
     s->tiles_per_unit = saved;
     const hipError_t e = hipGetLastError();
     return e == hipSuccess ? SPIKE_OK : hip_fail(e, "stream launch");
@@ -906,8 +913,8 @@ int spike_stream_destroy(spike_stream_t s)
     hipError_t e = hipDeviceSynchronize();
     if (e != hipSuccess)
         rc = hip_fail(e, "hipDeviceSynchronize");
-    if (s->d_desc)
-        (void)hipFree(s->d_desc);
+    if (s->d_ops)
+        (void)hipFree(s->d_ops);
     delete s;
     return rc;
 }

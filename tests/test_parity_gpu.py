@@ -455,7 +455,7 @@ def test_every_instantiated_shape(sp, K, N):
             sp.spike_proj_tune(h, sp.SPIKE_TUNE_TILES_PER_UNIT, tpu)
             assert_parity(sp, h, p["W"], p["scale"], p["masks"])
         ran += 1
-    assert ran >= 10
+    assert ran == sum(N % decode_shape(c)["V"] == 0 for c in sp.spike_proj_shapes())
 
 
 def test_stream_every_shape_and_xcd_spread(sp, stack):
