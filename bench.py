@@ -43,7 +43,11 @@ DEFAULT_SETS = 32          # rotated weight copies of the decode stack (8.3 GB)
 DEFAULT_TOKENS = 1000
 METRIC = "active-column INT8 GB/s (% HBM peak) + per-token 22-layer spike-proj latency"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_stream_decode_stack_traffic.json")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_03026_amd", "csrc", f) for f in ("gather.hpp", "spike_proj.hip")]
+# The timed kernel: the stream kernel of gather.hpp at this launch shape
+# (16 bytes per lane, 32-lane groups, 4 columns in flight, 256 threads,
+# nontemporal loads).  The traffic record is keyed on both.
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_03026_amd", "csrc", "gather.hpp")]
+HEADLINE_SHAPE = (16, 32, 4, 256, True)
 
 
 def log(msg: str) -> None:
@@ -51,9 +55,11 @@ def log(msg: str) -> None:
 
 
 def kernel_source_hash() -> str:
+    """Hash of the device code the headline kernel is built from, and of its launch shape."""
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
         h.update(open(p, "rb").read())
+    h.update(repr(HEADLINE_SHAPE).encode())
     return h.hexdigest()[:16]
 
 
@@ -99,36 +105,44 @@ def graph_of(torch, fn):
     return g
 
 
-def make_handles(sp, torch, host, copies: int):
+def make_handles(sp, torch, host, copies: int, max_B: int = 1):
     """Device weights and handles for (W, scale) pairs, plus `copies` - 1
-    address-distinct device copies of all of them."""
+    address-distinct device copies of all of them.  Handles hold a workspace
+    for max_B rows (no matrix-core copy of W below the matrix-core minimum)."""
     dev = [(torch.from_numpy(W).cuda(), torch.from_numpy(s).cuda()) for (W, s) in host]
-    base = [sp.spike_proj_create(W, s) for (W, s) in dev]
+    base = [sp.spike_proj_create_reserved(W, s, max_B) for (W, s) in dev]
     extra = []
     for _ in range(copies - 1):
         for (W, s) in dev:
-            h = sp.spike_proj_create(W.clone(), s.clone())
-            sp.spike_proj_reserve(h, 1)
-            extra.append(h)
+            extra.append(sp.spike_proj_create_reserved(W.clone(), s.clone(), 1))
     return base, extra
 
 
-def cpu_baseline(host, masks, Ks, budget_s: float, threads: int):
-    """The oracle, as it stands, on the first tokens of the same stream until
-    about budget_s seconds of CPU work are done."""
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(host, masks, Ks, n_tokens: int, threads: int, passes: int = 5):
+    """The oracle, as it stands, on the first n_tokens tokens of the same
+    stream: one call per projection over all sampled rows.  Returns the
+    median rate over `passes` passes, in active-column GB/s."""
     import oracle
     offs = np.cumsum([0] + [(K + 63) // 64 for K in Ks])
-    done_bytes, t0, tokens = 0, time.perf_counter(), 0
-    for t in range(masks.shape[0]):
+    sample = masks[:n_tokens]
+    active_bytes = int(active_counts(sample, Ks).sum()) * host[0][0].shape[1]
+    times = []
+    for _ in range(passes):
+        t0 = time.perf_counter()
         for j, (W, s) in enumerate(host):
-            m = masks[t:t + 1, offs[j]:offs[j + 1]]
-            oracle.spike_forward(W, s, m, threads=threads)
-            done_bytes += int(np.unpackbits(m.view(np.uint8), bitorder="little")[:Ks[j]].sum()) * W.shape[1]
-        tokens += 1
-        if time.perf_counter() - t0 >= budget_s:
-            break
-    el = time.perf_counter() - t0
-    return done_bytes / el / 1e9, tokens, el
+            oracle.spike_forward(W, s, sample[:, offs[j]:offs[j + 1]], threads=threads)
+        times.append(time.perf_counter() - t0)
+    return active_bytes / float(np.median(times)) / 1e9, float(np.median(times))
 
 
 def bench_decode_stack(sp, torch, wl, timer, args):
@@ -146,6 +160,8 @@ def bench_decode_stack(sp, torch, wl, timer, args):
     out = torch.empty((T, len(order) * N), dtype=torch.float32, device="cuda")
     cold = sp.spike_stream_create(handles + copies, len(order), R, T)
     warm = sp.spike_stream_create(handles, len(order), 1, T)
+    for st in (cold, warm):
+        sp.spike_stream_tune(st, sp.SPIKE_TUNE_SHAPE, sp.SPIKE_SHAPE(*HEADLINE_SHAPE))
     torch.cuda.synchronize()
 
     sec = timer(lambda: sp.spike_stream_forward(cold, dmasks, out), args.steps, args.warmup)
@@ -153,7 +169,7 @@ def bench_decode_stack(sp, torch, wl, timer, args):
     log(f"stream cold: {sec * 1e3:.3f} ms/step, {gbs:.1f} GB/s active-column ({100 * gbs / HBM_PEAK_GBS:.1f}% of HBM)")
     sec_w = timer(lambda: sp.spike_stream_forward(warm, dmasks, out), max(3, args.steps // 2), 1)
     warm_gbs = step_bytes / sec_w / 1e9
-    log(f"stream warm: {warm_gbs:.1f} GB/s")
+    log(f"stream warm (one weight set, {R}x fewer bytes than the cold copies): {warm_gbs:.1f} GB/s")
     res = {"sec": sec, "gbs": gbs, "warm_gbs": warm_gbs, "step_bytes": step_bytes, "host": host, "masks": masks,
            "Ks": Ks}
 
@@ -194,36 +210,61 @@ def bench_decode_stack(sp, torch, wl, timer, args):
     return res
 
 
-def bench_batch1(sp, torch, wl, timer, name, d, sets: int, calls: int):
-    """One projection at batch 1: mean latency of `calls` dependent calls
-    (graph replay) and the stream rate over the same masks on `sets` rotated
-    weight copies."""
-    K, N = d["K"], d["N"]
-    masks = d["masks"]
-    nm = masks.shape[0]
-    counts = active_counts(masks, [K])[:, 0]
-    handles, copies = make_handles(sp, torch, [(d["W"], d["scale"])], sets)
+MALL_BYTES = 256 << 20  # MI355X Infinity Cache
+
+
+def bench_batch1(sp, torch, timer, name, W, scale, mask_sets, copies: int, warm_sets: int, calls: int):
+    """One projection at batch 1, for each (label, rate, masks) of mask_sets:
+    mean latency of `calls` dependent calls (graph replay, one weight copy),
+    and the stream rate over all masks, cold and warm.  Cold: mask i reads
+    copy i % copies, and `copies` is chosen so that the active-column bytes
+    read between two uses of a copy exceed the Infinity Cache.  Warm:
+    `warm_sets` copies, whose bytes stay in the caches."""
+    K, N = W.shape
+    handles, extra = make_handles(sp, torch, [(W, scale)], copies)
+    all_h = handles + extra
     h = handles[0]
-    dm = torch.from_numpy(masks.view(np.int64)).cuda()
-    out = torch.empty((nm, N), device="cuda")
-    n = min(calls, nm)
-    g = graph_of(torch, lambda: [sp.spike_proj_forward(h, dm[i], 1, out[i]) for i in range(n)])
-    sec = timer(g.replay, 3, 1) / n
-    st = sp.spike_stream_create(handles + copies, 1, sets, nm)
-    sec_s = timer(lambda: sp.spike_stream_forward(st, dm, out), 5, 1)
-    st.close()
-    bytes_per = float(counts.mean()) * N
-    r = {"K": K, "N": N, "p": d["p"], "active_bytes_mean": round(bytes_per), "call_us": round(sec * 1e6, 2),
-         "call_gbs": round(bytes_per / sec / 1e9, 1), "stream_gbs": round(counts.sum() * N / sec_s / 1e9, 1),
-         "stream_sets": sets, "masks": nm}
-    log(f"{name}: {r['call_us']} us per dependent call ({r['call_gbs']} GB/s); stream {r['stream_gbs']} GB/s")
-    return r
+    results = []
+    for label, p, masks in mask_sets:
+        nm = masks.shape[0]
+        counts = active_counts(masks, [K])[:, 0]
+        dm = torch.from_numpy(masks.view(np.int64)).cuda()
+        out = torch.empty((nm, N), device="cuda")
+        n = min(calls, nm)
+        g = graph_of(torch, lambda: [sp.spike_proj_forward(h, dm[i], 1, out[i]) for i in range(n)])
+        sec = timer(g.replay, 3, 1) / n
+        del g
+        rates = {}
+        for kind, hs in (("cold", all_h), ("warm", all_h[:warm_sets])):
+            st = sp.spike_stream_create(hs, 1, len(hs), nm)
+            sec_s = timer(lambda: sp.spike_stream_forward(st, dm, out), 5, 1)
+            st.close()
+            rates[kind] = round(counts.sum() * N / sec_s / 1e9, 1)
+        bytes_per = float(counts.mean()) * N
+        r = {"K": K, "N": N, "p": p, "active_bytes_mean": round(bytes_per), "call_us": round(sec * 1e6, 2),
+             "call_gbs": round(bytes_per / sec / 1e9, 1), "stream_masks": nm, "stream_gbs_cold": rates["cold"],
+             "stream_hbm_frac_cold": round(rates["cold"] / HBM_PEAK_GBS, 4), "stream_cold_copies": copies,
+             "cold_reuse_distance_bytes": int(bytes_per * copies), "stream_gbs_warm": rates["warm"],
+             "stream_warm_copies": warm_sets}
+        log(f"{name} {label}: {r['call_us']} us per dependent call ({r['call_gbs']} GB/s); stream over {nm} masks: "
+            f"cold {r['stream_gbs_cold']} GB/s ({100 * r['stream_hbm_frac_cold']:.1f}% of HBM), "
+            f"warm {r['stream_gbs_warm']} GB/s")
+        results.append(r)
+    for x in all_h:
+        x.close()
+    return results
+
+
+def cold_copies(bytes_per_mask: float, n_masks: int) -> int:
+    """Weight copies for a cold stream: the active bytes read between two
+    uses of one copy are at least twice the Infinity Cache."""
+    return int(min(n_masks, max(32, np.ceil(2 * MALL_BYTES / bytes_per_mask))))
 
 
 def bench_prefill(sp, torch, wl, timer):
     d = wl.prefill_projection()
     B, K, N = d["masks"].shape[0], d["K"], d["N"]
-    h = make_handles(sp, torch, [(d["W"], d["scale"])], 1)[0][0]
+    h = make_handles(sp, torch, [(d["W"], d["scale"])], 1, max_B=B)[0][0]
     dm = torch.from_numpy(d["masks"].view(np.int64)).cuda()
     out = torch.empty((B, N), device="cuda")
     r = {"B": B, "K": K, "N": N}
@@ -244,7 +285,7 @@ def bench_batched_stack(sp, torch, wl, timer, steps: int = 16, B: int = 64):
     order = wl.stack_order()
     host = [wl.batched_stack_projection(l, j) for (l, j) in order]
     bits = [wl.batched_stack_bits(l, j, B=B, n_steps=steps) for (l, j) in order]
-    handles = make_handles(sp, torch, host, 1)[0]
+    handles = make_handles(sp, torch, host, 1, max_B=B)[0]
     per_step = [np.concatenate([wl.pack_bits(b[s]).reshape(-1) for b in bits]) for s in range(steps)]
     union = sum(int(b.any(axis=1).sum(axis=1).mean()) * 1536 for b in bits)  # mean union columns per step
     dm = [torch.from_numpy(m.view(np.int64)).cuda() for m in per_step]
@@ -287,7 +328,8 @@ def main(argv=None) -> int:
     ap.add_argument("--tokens", type=int, default=DEFAULT_TOKENS)
     ap.add_argument("--sets", type=int, default=DEFAULT_SETS)
     ap.add_argument("--latency-tokens", type=int, default=1000)
-    ap.add_argument("--cpu-budget", type=float, default=8.0, help="seconds per CPU-baseline leg")
+    ap.add_argument("--batch1-masks", type=int, default=8000, help="masks per batch-1 stream (configs 1-2)")
+    ap.add_argument("--cpu-tokens", type=int, default=100, help="tokens of the stream in the CPU-baseline sample")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-latency", action="store_true")
     ap.add_argument("--only-stream", action="store_true", help="time only the headline stream (for profiling)")
@@ -322,27 +364,36 @@ def main(argv=None) -> int:
 
     extra = {}
     if not args.only_stream:
-        extra["single_1536x1536_b1"] = bench_batch1(sp, torch, wl, timer, "1536x1536 p=0.10",
-                                                    wl.single_projection(n_masks=1000), 32, 1000)
-        extra["down_6144x1536_b1"] = [
-            bench_batch1(sp, torch, wl, timer, f"6144x1536 p={p}", wl.down_sweep(p, n_masks=1000), 32, 200)
-            for p in wl.DOWN_SWEEP_RATES]
+        nm = args.batch1_masks
+        d = wl.single_projection(n_masks=nm)
+        copies = cold_copies(0.10 * d["K"] * d["N"], nm)
+        extra["single_1536x1536_b1"] = bench_batch1(sp, torch, timer, "1536x1536", d["W"], d["scale"],
+                                                    [("p=0.10", d["p"], d["masks"])], copies, 32, 1000)[0]
+        downs = [wl.down_sweep(p, n_masks=nm) for p in wl.DOWN_SWEEP_RATES]
+        copies = cold_copies(min(wl.DOWN_SWEEP_RATES) * downs[0]["K"] * downs[0]["N"], nm)
+        extra["down_6144x1536_b1"] = bench_batch1(sp, torch, timer, "6144x1536", downs[0]["W"], downs[0]["scale"],
+                                                  [(f"p={x['p']}", x["p"], x["masks"]) for x in downs], copies, 32,
+                                                  200)
+        del downs
         extra["prefill_512x6144x1536"] = bench_prefill(sp, torch, wl, timer)
         extra["batched_stack_b64"] = bench_batched_stack(sp, torch, wl, timer)
 
     cpu = None
     if not args.no_cpu:
-        cores = min(len(os.sched_getaffinity(0)), 16)
+        affinity = len(os.sched_getaffinity(0))
+        threads = min(affinity, 16)  # the host share of one GPU on the box
         host, masks, Ks = main_res["host"], main_res["masks"], main_res["Ks"]
-        v1, tok1, el1 = cpu_baseline(host, masks, Ks, args.cpu_budget, 1)
-        vn, tokn, eln = cpu_baseline(host, masks, Ks, args.cpu_budget, cores)
+        nt = args.cpu_tokens
+        v1, t1 = cpu_baseline(host, masks, Ks, nt, 1)
+        vn, tn = cpu_baseline(host, masks, Ks, nt, threads)
         best_multi = vn >= v1
-        cpu = {"value": round(max(v1, vn), 3), "unit": "GB/s", "cores": cores if best_multi else 1,
+        cpu = {"value": round(max(v1, vn), 3), "unit": "GB/s", "cores": threads if best_multi else 1,
                "kind": "oracle",
-               "sample": (f"first {tokn if best_multi else tok1} tokens x 44 projections of the same stream "
-                          f"({eln if best_multi else el1:.1f} s); 1 thread: {v1:.3f} GB/s over {tok1} tokens, "
-                          f"{cores} threads: {vn:.3f} GB/s over {tokn} tokens")}
-        log(f"cpu oracle: {v1:.3f} GB/s on 1 thread, {vn:.3f} GB/s on {cores}")
+               "sample": (f"first {nt} tokens x 44 projections of the same stream, one oracle call per projection "
+                          f"over the {nt} rows, median of 5 passes; 1 thread: {v1:.3f} GB/s ({t1:.2f} s per pass), "
+                          f"{threads} threads: {vn:.3f} GB/s ({tn:.2f} s per pass); host CPU {cpu_model()}, "
+                          f"{affinity} cores in the process affinity mask")}
+        log(f"cpu oracle: {v1:.3f} GB/s on 1 thread, {vn:.3f} GB/s on {threads} ({cpu_model()})")
 
     traffic = traffic_record()
     rec = {
@@ -367,8 +418,9 @@ def main(argv=None) -> int:
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gbs / HBM_PEAK_GBS, 4),
                      "traffic": None if traffic is None else traffic["hbm_bytes_per_launch"],
-                     "kernel": "k_stream (one launch per step)", "kernel_source_hash": kernel_source_hash()},
-        "warm_gbs": round(main_res["warm_gbs"], 1),
+                     "kernel": f"k_stream<Shape{HEADLINE_SHAPE}> (one launch per step)",
+                     "kernel_source_hash": kernel_source_hash()},
+        "warm_one_set_gbs": round(main_res["warm_gbs"], 1),
         "per_token_latency": main_res.get("latency"),
         "workloads": extra,
         "cpu_baseline": cpu,

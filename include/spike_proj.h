@@ -74,6 +74,14 @@ typedef struct spike_stream *spike_stream_t;
 int spike_proj_create(const int8_t *W_int8_colmajor, const float *scale_fp32, int32_t K, int32_t N,
                       spike_proj_t *out_handle);
 
+/* spike_proj_create with the workspace sized for max_B rows (1 <= max_B <=
+ * 65535) instead of SPIKE_DEFAULT_MAX_B.  Below the matrix-core minimum
+ * batch (SPIKE_TUNE_MFMA_MIN_B, default 5) no matrix-core copy of W is made:
+ * handles meant for batch-1 calls or streams then hold only a workspace of
+ * max_B * N INT32 entries and never a second copy of the weights. */
+int spike_proj_create_reserved(const int8_t *W_int8_colmajor, const float *scale_fp32, int32_t K, int32_t N,
+                               int32_t max_B, spike_proj_t *out_handle);
+
 /* Resize the workspace so that forward() accepts up to max_B rows
  * (1 <= max_B <= 65535).  A max_B below the matrix-core minimum batch
  * (SPIKE_TUNE_MFMA_MIN_B, default 5) also frees the matrix-core copy of W,

@@ -108,85 +108,92 @@ int oracle_spike_acc(const int8_t *W, int64_t K, int64_t N, const uint64_t *mask
 struct range_job {
     const int8_t *W;
     const float *scale;
-    int64_t N;
-    const int32_t *active;
-    int64_t n_active;
+    const uint64_t *mask;
+    int64_t K, N, B, words;
     int64_t n0, n1;
     float *out;
     int status;
 };
 
+/* One thread's share of oracle_spike_forward: output channels [n0, n1) of
+ * every row, each row computed by the three steps above. */
 static void *run_range(void *arg)
 {
     struct range_job *job = (struct range_job *)arg;
     int64_t width = job->n1 - job->n0;
+    int32_t *active = (int32_t *)malloc(sizeof(int32_t) * (size_t)job->K);
     int32_t *acc = (int32_t *)malloc(sizeof(int32_t) * (size_t)(width > 0 ? width : 1));
-    if (!acc) {
+    if (!active || !acc) {
+        free(active);
+        free(acc);
         job->status = -3;
         return NULL;
     }
-    accumulate_active_columns(job->W, job->N, job->active, job->n_active, job->n0, job->n1, acc);
-    for (int64_t n = job->n0; n < job->n1; ++n)
-        job->out[n] = scale_once(acc[n - job->n0], job->scale[n]);
+    for (int64_t b = 0; b < job->B; ++b) {
+        int64_t n_active = oracle_active_indices(job->mask + b * job->words, job->K, active);
+        accumulate_active_columns(job->W, job->N, active, n_active, job->n0, job->n1, acc);
+        float *out_row = job->out + b * job->N;
+        for (int64_t n = job->n0; n < job->n1; ++n)
+            out_row[n] = scale_once(acc[n - job->n0], job->scale[n]);
+    }
+    free(active);
     free(acc);
     job->status = 0;
     return NULL;
 }
 
 /* FP32 outputs for B spike rows: out[b*N + n] = fl32(fl32(acc) * scale[n]).
- * With threads > 1 each thread owns a contiguous range of output channels and
- * walks the same active list, so the result does not depend on the thread
- * count.  Returns 0, -1 on bad arguments, -3 when memory runs out. */
+ * With threads > 1 each thread owns a contiguous range of output channels of
+ * every row and walks the same active lists, so the result does not depend
+ * on the thread count.  Returns 0, -1 on bad arguments, -3 when memory runs
+ * out. */
 int oracle_spike_forward(const int8_t *W, const float *scale, int64_t K, int64_t N,
                          const uint64_t *mask, int64_t B, float *out, int threads)
 {
     if (check_args(W, mask, K, N, B, out) || (B > 0 && !scale))
         return -1;
+    if (B == 0)
+        return 0;
     if (threads < 1)
         threads = 1;
     if (threads > N)
         threads = (int)N;
-    const int64_t words = (K + 63) / 64;
-    int32_t *active = (int32_t *)malloc(sizeof(int32_t) * (size_t)K);
     struct range_job *jobs = (struct range_job *)calloc((size_t)threads, sizeof(struct range_job));
     pthread_t *tids = (pthread_t *)calloc((size_t)threads, sizeof(pthread_t));
     int status = 0;
-    if (!active || !jobs || !tids) {
+    if (!jobs || !tids) {
         status = -3;
         goto done;
     }
-    for (int64_t b = 0; b < B && status == 0; ++b) {
-        int64_t n_active = oracle_active_indices(mask + b * words, K, active);
-        for (int t = 0; t < threads; ++t) {
-            jobs[t].W = W;
-            jobs[t].scale = scale;
-            jobs[t].N = N;
-            jobs[t].active = active;
-            jobs[t].n_active = n_active;
-            jobs[t].n0 = N * t / threads;
-            jobs[t].n1 = N * (t + 1) / threads;
-            jobs[t].out = out + b * N;
-            jobs[t].status = -3;
-        }
-        if (threads == 1) {
-            run_range(&jobs[0]);
-        } else {
-            int started = 0;
-            for (int t = 0; t < threads; ++t, ++started)
-                if (pthread_create(&tids[t], NULL, run_range, &jobs[t]) != 0)
-                    break;
-            for (int t = 0; t < started; ++t)
-                pthread_join(tids[t], NULL);
-            if (started < threads)
-                for (int t = started; t < threads; ++t)
-                    run_range(&jobs[t]);
-        }
-        for (int t = 0; t < threads; ++t)
-            if (jobs[t].status != 0)
-                status = jobs[t].status;
+    for (int t = 0; t < threads; ++t) {
+        jobs[t].W = W;
+        jobs[t].scale = scale;
+        jobs[t].mask = mask;
+        jobs[t].K = K;
+        jobs[t].N = N;
+        jobs[t].B = B;
+        jobs[t].words = (K + 63) / 64;
+        jobs[t].n0 = N * t / threads;
+        jobs[t].n1 = N * (t + 1) / threads;
+        jobs[t].out = out;
+        jobs[t].status = -3;
     }
+    if (threads == 1) {
+        run_range(&jobs[0]);
+    } else {
+        int started = 0;
+        for (int t = 0; t < threads; ++t, ++started)
+            if (pthread_create(&tids[t], NULL, run_range, &jobs[t]) != 0)
+                break;
+        for (int t = 0; t < started; ++t)
+            pthread_join(tids[t], NULL);
+        for (int t = started; t < threads; ++t)
+            run_range(&jobs[t]);
+    }
+    for (int t = 0; t < threads; ++t)
+        if (jobs[t].status != 0)
+            status = jobs[t].status;
 done:
-    free(active);
     free(jobs);
     free(tids);
     return status;

@@ -32,7 +32,7 @@ EXPORTED = (
     "spike_proj_destroy", "spike_proj_tune", "spike_compact", "spike_stack_forward",
     "spike_stream_create", "spike_stream_forward", "spike_stream_tune", "spike_stream_destroy",
     "spike_proj_last_error", "spike_proj_shapes", "spike_mfma_plans", "spike_proj_plan_query",
-    "spike_proj_abi_version", "spike_proj_forward_noalloc",
+    "spike_proj_abi_version", "spike_proj_forward_noalloc", "spike_proj_create_reserved",
 )
 
 if not os.path.exists(LIB):
@@ -42,6 +42,7 @@ _lib = ctypes.CDLL(LIB)
 _p, _i32 = ctypes.c_void_p, ctypes.c_int32
 _sig = {
     "spike_proj_create": [_p, _p, _i32, _i32, ctypes.POINTER(_p)],
+    "spike_proj_create_reserved": [_p, _p, _i32, _i32, _i32, ctypes.POINTER(_p)],
     "spike_proj_reserve": [_p, _i32],
     "spike_proj_forward": [_p, _p, _i32, _p, _p],
     "spike_proj_forward_acc": [_p, _p, _i32, _p, _p],
@@ -118,16 +119,31 @@ class SpikeProj:
             pass
 
 
-def spike_proj_create(W: torch.Tensor, scale: torch.Tensor) -> SpikeProj:
-    """W: int8 [K, N] (column-major storage of the [N, K] weight), scale: float32 [N]."""
+def _check_operands(W: torch.Tensor, scale: torch.Tensor) -> None:
     if W.dtype != torch.int8 or W.dim() != 2:
         raise TypeError("W must be an int8 tensor [K, N]")
     if scale.dtype != torch.float32 or scale.shape != (W.shape[1],):
         raise TypeError(f"scale must be float32 [N={W.shape[1]}]")
+
+
+def spike_proj_create(W: torch.Tensor, scale: torch.Tensor) -> SpikeProj:
+    """W: int8 [K, N] (column-major storage of the [N, K] weight), scale: float32 [N]."""
+    _check_operands(W, scale)
     out = _p()
     _check(_lib.spike_proj_create(_dev_ptr(W, "W"), _dev_ptr(scale, "scale"), W.shape[0], W.shape[1],
                                   ctypes.byref(out)), "spike_proj_create")
     return SpikeProj(out.value, W, scale)
+
+
+def spike_proj_create_reserved(W: torch.Tensor, scale: torch.Tensor, max_B: int) -> SpikeProj:
+    """spike_proj_create with a workspace for max_B rows (no matrix-core copy below the minimum batch)."""
+    _check_operands(W, scale)
+    out = _p()
+    _check(_lib.spike_proj_create_reserved(_dev_ptr(W, "W"), _dev_ptr(scale, "scale"), W.shape[0], W.shape[1],
+                                           int(max_B), ctypes.byref(out)), "spike_proj_create_reserved")
+    h = SpikeProj(out.value, W, scale)
+    h.max_B = int(max_B)
+    return h
 
 
 def spike_proj_reserve(h: SpikeProj, max_B: int) -> None:
@@ -156,11 +172,8 @@ SPIKE_STATIC_SCRATCH_WORDS = 1 << 20
 def spike_proj_forward_noalloc(W: torch.Tensor, scale: torch.Tensor, mask: torch.Tensor, B: int, out: torch.Tensor,
                                stream=None) -> None:
     """Handle-free forward on the library's static scratch (no device allocation)."""
-    if W.dtype != torch.int8 or W.dim() != 2:
-        raise TypeError("W must be an int8 tensor [K, N]")
+    _check_operands(W, scale)
     K, N = W.shape
-    if scale.dtype != torch.float32 or scale.shape != (N,):
-        raise TypeError(f"scale must be float32 [N={N}]")
     if out.dtype != torch.float32:
         raise TypeError("out must be float32")
     _check(_lib.spike_proj_forward_noalloc(_dev_ptr(W, "W"), _dev_ptr(scale, "scale"), int(K), int(N),

@@ -496,7 +496,8 @@ int static_scratch(int dev, hipStream_t st, uint32_t** out)
 
 extern "C" {
 
-int spike_proj_create(const int8_t* W, const float* scale, int32_t K, int32_t N, spike_proj_t* out_handle)
+int spike_proj_create_reserved(const int8_t* W, const float* scale, int32_t K, int32_t N, int32_t max_B,
+                               spike_proj_t* out_handle)
 {
     g_last_error.clear();
     if (!out_handle)
@@ -508,6 +509,8 @@ int spike_proj_create(const int8_t* W, const float* scale, int32_t K, int32_t N,
         return fail(SPIKE_EINVAL, "K = %d outside [1, %d]", K, SPIKE_MAX_K);
     if (N < 1 || N > SPIKE_MAX_N)
         return fail(SPIKE_EINVAL, "N = %d outside [1, %d]", N, SPIKE_MAX_N);
+    if (max_B < 1 || max_B > 65535)
+        return fail(SPIKE_EINVAL, "max_B = %d outside [1, 65535]", max_B);
     spike_proj* h = new (std::nothrow) spike_proj;
     if (!h)
         return fail(SPIKE_ENOMEM, "handle allocation failed");
@@ -522,18 +525,26 @@ int spike_proj_create(const int8_t* W, const float* scale, int32_t K, int32_t N,
         delete h;
         return hip_fail(e, "hipGetDevice");
     }
-    if (int rc = alloc_workspace(h, SPIKE_DEFAULT_MAX_B)) {
+    if (int rc = alloc_workspace(h, max_B)) {
         delete h;
         return rc;
     }
-    if (int rc = make_packed(h)) {
-        (void)hipFree(h->ws);
-        (void)hipFree(h->counters);
-        delete h;
-        return rc;
+    // the matrix-core copy of W only where batches that use it can be run
+    if (max_B >= h->mfma_min_b) {
+        if (int rc = make_packed(h)) {
+            (void)hipFree(h->ws);
+            (void)hipFree(h->counters);
+            delete h;
+            return rc;
+        }
     }
     *out_handle = h;
     return SPIKE_OK;
+}
+
+int spike_proj_create(const int8_t* W, const float* scale, int32_t K, int32_t N, spike_proj_t* out_handle)
+{
+    return spike_proj_create_reserved(W, scale, K, N, SPIKE_DEFAULT_MAX_B, out_handle);
 }
 
 int spike_proj_reserve(spike_proj_t h, int32_t max_B)
