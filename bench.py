@@ -292,10 +292,12 @@ def bench_batched_stack(sp, torch, wl, timer, steps: int = 16, B: int = 64):
     static = torch.zeros_like(dm[0])
     out = torch.empty(sum(B * h.N for h in handles), device="cuda")
     r = {"B": B, "steps": steps, "union_bytes_per_step": union}
-    for name, path in (("mfma", sp.SPIKE_PATH_AUTO), ("gather", sp.SPIKE_PATH_GATHER)):
+    for name, path, fn in (("fused", sp.SPIKE_PATH_AUTO, sp.spike_stack_forward_fused),
+                           ("mfma", sp.SPIKE_PATH_AUTO, sp.spike_stack_forward),
+                           ("gather", sp.SPIKE_PATH_GATHER, sp.spike_stack_forward)):
         for h in handles:
             sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, path)
-        g = graph_of(torch, lambda: sp.spike_stack_forward(handles, static, B, out))
+        g = graph_of(torch, lambda: fn(handles, static, B, out))
         times = []
         for s in range(steps):
             static.copy_(dm[s])
@@ -303,8 +305,9 @@ def bench_batched_stack(sp, torch, wl, timer, steps: int = 16, B: int = 64):
         t = float(np.median(times))
         r[f"{name}_step_us"] = round(t * 1e6, 1)
         r[f"{name}_union_gbs"] = round(union / t / 1e9, 1)
-    log(f"batched stack B={B}: matrix cores {r['mfma_step_us']} us/step ({r['mfma_union_gbs']} GB/s on union "
-        f"bytes), gather {r['gather_step_us']} us/step")
+    log(f"batched stack B={B}: one fused matrix-core launch per step {r['fused_step_us']} us/step "
+        f"({r['fused_union_gbs']} GB/s on union bytes); in stream order (44 launches): matrix cores "
+        f"{r['mfma_step_us']} us/step, gather {r['gather_step_us']} us/step")
     return r
 
 

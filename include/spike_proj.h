@@ -228,6 +228,21 @@ int spike_compact(const uint64_t *spike_bitmask, int32_t B, int32_t K, int32_t *
 int spike_stack_forward(const spike_proj_t *projs, int32_t n_proj, const uint64_t *masks, int32_t B,
                         float *out, void *stream);
 
+/* The projections of spike_stack_forward (same arguments, same mask and
+ * output layout) in ONE launch on the matrix cores, for callers whose spike
+ * inputs are all given up front: no projection's input may depend on an
+ * earlier projection's output in the same call (Sec. 2.1: a block's TCAM and
+ * down projections, 22 blocks).  One launch instead of n_proj removes the
+ * per-launch latency that dominates batched decode (a 1536 x 1536 projection
+ * at B = 64 reads 2.4 MB, well under a microsecond at HBM rate).  Requires,
+ * for every handle: the same N (a multiple of 16), a matrix-core copy of W
+ * (a reserved batch of at least the matrix-core minimum), B rows reserved;
+ * at most 64 projections.  Returns SPIKE_EUNSUPPORTED where these do not
+ * hold (spike_stack_forward then serves the call).  Results are identical
+ * to spike_stack_forward's. */
+int spike_stack_forward_fused(const spike_proj_t *projs, int32_t n_proj, const uint64_t *masks, int32_t B,
+                              float *out, void *stream);
+
 /* Throughput mode for many independent batch-1 projections: n_tokens
  * tokens, each running n_proj projections, all in one launch.  projs holds
  * n_sets * n_proj handles; token t uses projs[(t % n_sets) * n_proj + j]

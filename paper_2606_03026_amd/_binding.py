@@ -33,6 +33,7 @@ EXPORTED = (
     "spike_stream_create", "spike_stream_forward", "spike_stream_tune", "spike_stream_destroy",
     "spike_proj_last_error", "spike_proj_shapes", "spike_mfma_plans", "spike_proj_plan_query",
     "spike_proj_abi_version", "spike_proj_forward_noalloc", "spike_proj_create_reserved",
+    "spike_stack_forward_fused",
 )
 
 if not os.path.exists(LIB):
@@ -51,6 +52,7 @@ _sig = {
     "spike_proj_tune": [_p, _i32, _i32],
     "spike_compact": [_p, _i32, _i32, _p, _p, _p],
     "spike_stack_forward": [_p, _i32, _p, _i32, _p, _p],
+    "spike_stack_forward_fused": [_p, _i32, _p, _i32, _p, _p],
     "spike_stream_create": [_p, _i32, _i32, _i32, ctypes.POINTER(_p)],
     "spike_stream_forward": [_p, _p, _p, _p],
     "spike_stream_tune": [_p, _i32, _i32],
@@ -211,6 +213,15 @@ def spike_stack_forward(handles, masks: torch.Tensor, B: int, out: torch.Tensor,
     ofl = sum(B * h.N for h in handles)
     _check(_lib.spike_stack_forward(arr, len(handles), _dev_ptr(masks, "masks", mwords * 8), int(B),
                                     _dev_ptr(out, "out", ofl * 4), _stream(stream)), "spike_stack_forward")
+
+
+def spike_stack_forward_fused(handles, masks: torch.Tensor, B: int, out: torch.Tensor, stream=None) -> None:
+    """All projections in one matrix-core launch (inputs all given); same layout as spike_stack_forward."""
+    arr = _handle_array(handles)
+    mwords = sum(B * words_per_row(h.K) for h in handles)
+    ofl = sum(B * h.N for h in handles)
+    _check(_lib.spike_stack_forward_fused(arr, len(handles), _dev_ptr(masks, "masks", mwords * 8), int(B),
+                                          _dev_ptr(out, "out", ofl * 4), _stream(stream)), "spike_stack_forward_fused")
 
 
 class SpikeStream:

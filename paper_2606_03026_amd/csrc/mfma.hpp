@@ -129,11 +129,12 @@ inline int mfma_lds_bytes(int RT, int CS, int wpr)
     return RT * CS * 256 * (int)sizeof(int32_t) + 16 * RT * mfma_stage_pitch(wpr) * (int)sizeof(uint64_t);
 }
 
+// One output tile (tile id `id` of the launch's n_rowtiles x n_coltiles
+// tiles) of one projection.
 template <int RT, int CS, int KW, int D, bool PRELOAD, bool ACC>
-__global__ __launch_bounds__(64 * KW) void k_mfma(const int8_t* __restrict__ P, const float* __restrict__ scale,
-                                                  int N, const uint64_t* __restrict__ mask, int wpr, int B,
-                                                  int n_rowtiles, int n_coltiles, float* __restrict__ out,
-                                                  int32_t* __restrict__ acc_out)
+__device__ inline void mfma_tile(const int8_t* __restrict__ P, const float* __restrict__ scale, int N,
+                                 const uint64_t* __restrict__ mask, int wpr, int B, int n_rowtiles, int n_coltiles,
+                                 int id, float* __restrict__ out, int32_t* __restrict__ acc_out)
 {
     constexpr int BLOCK = 64 * KW;
     constexpr int ROWS = 16 * RT;
@@ -150,7 +151,7 @@ __global__ __launch_bounds__(64 * KW) void k_mfma(const int8_t* __restrict__ P, 
     const int q = l / 16;  // k-group of the operands, row group of the result
     const int c = l % 16;  // row of A, channel of B and of the result
     int ct, rt;
-    mfma_tile_of(blockIdx.x, n_rowtiles, n_coltiles, &ct, &rt);
+    mfma_tile_of(id, n_rowtiles, n_coltiles, &ct, &rt);
     const int m0 = rt * ROWS;
     const int t0 = ct * CS;  // first channel set of the tile
 
@@ -332,6 +333,44 @@ __global__ __launch_bounds__(64 * KW) void k_mfma(const int8_t* __restrict__ P, 
     }
 }
 
+template <int RT, int CS, int KW, int D, bool PRELOAD, bool ACC>
+__global__ __launch_bounds__(64 * KW) void k_mfma(const int8_t* __restrict__ P, const float* __restrict__ scale,
+                                                  int N, const uint64_t* __restrict__ mask, int wpr, int B,
+                                                  int n_rowtiles, int n_coltiles, float* __restrict__ out,
+                                                  int32_t* __restrict__ acc_out)
+{
+    mfma_tile<RT, CS, KW, D, PRELOAD, ACC>(P, scale, N, mask, wpr, B, n_rowtiles, n_coltiles, blockIdx.x, out,
+                                           acc_out);
+}
+
+// Several projections of B given spike rows each, in one launch: item j
+// (packed weights P[j], scales, K_j) reads its rows at word mask_off[j] of
+// the mask buffer and writes its outputs at float out_off[j].  Every item
+// has the same N and B, so the same tile count; workgroup b runs tile
+// b % tiles of item b / tiles.  (Tiles per item are a multiple of 8 when
+// the channel tiles are, so the XCD grouping of mfma_tile_of holds per
+// item.)  The ring form serves any k-step count.
+constexpr int kMfmaMaxItems = 64;
+struct MfmaItems {
+    const int8_t* P[kMfmaMaxItems];
+    const float* scale[kMfmaMaxItems];
+    int64_t mask_off[kMfmaMaxItems];
+    int64_t out_off[kMfmaMaxItems];
+    int32_t wpr[kMfmaMaxItems];
+};
+
+template <int RT, int CS, int KW, int D>
+__global__ __launch_bounds__(64 * KW) void k_mfma_items(const MfmaItems items, int N, const uint64_t* __restrict__ mask,
+                                                        int B, int n_rowtiles, int n_coltiles, float* __restrict__ out)
+{
+    const int tiles = n_rowtiles * n_coltiles;
+    const int item = blockIdx.x / tiles;
+    const int id = blockIdx.x - item * tiles;
+    mfma_tile<RT, CS, KW, D, false, false>(items.P[item], items.scale[item], N, mask + items.mask_off[item],
+                                           items.wpr[item], B, n_rowtiles, n_coltiles, id, out + items.out_off[item],
+                                           nullptr);
+}
+
 // Launch configuration of the matrix-core path.
 struct MfmaPlan {
     int rt, cs, kw, d;
@@ -354,7 +393,9 @@ struct MfmaPlan {
     X(8, 2, 8, 4, false) X(4, 6, 8, 2, false) X(4, 3, 16, 2, false) X(4, 3, 16, 4, false) X(4, 2, 16, 4, false)  \
     X(2, 3, 16, 4, false) X(1, 2, 1, 4, true) X(1, 2, 2, 4, true) X(1, 2, 16, 4, false) X(1, 1, 16, 2, false)    \
     X(1, 2, 16, 2, false) X(1, 3, 16, 2, false) X(2, 1, 16, 2, false) X(2, 2, 16, 2, false) X(2, 3, 16, 2, false) \
-    X(4, 1, 16, 2, false) X(4, 2, 16, 2, false)
+    X(4, 1, 16, 2, false) X(4, 2, 16, 2, false) X(1, 1, 1, 4, false) X(1, 2, 1, 4, false) X(1, 1, 2, 4, false)    \
+    X(1, 2, 2, 4, false) X(1, 1, 4, 4, false) X(1, 2, 4, 4, false) X(4, 1, 1, 2, false) X(4, 3, 1, 2, false)     \
+    X(4, 1, 2, 2, false) X(4, 3, 2, 2, false)
 
 inline bool mfma_instantiated(const MfmaPlan& p)
 {
@@ -427,6 +468,31 @@ inline MfmaPlan mfma_plan(int K, int N, int B, int rt_req, int cs_req, int kw_re
     return p;
 }
 
+// A ring plan (any k-step count) for a launch whose projections all have
+// at least min_wpr k-steps: the instantiated ring plan with p's row tile
+// and a channel-set count dividing N / 16, preferring p's channel sets,
+// then the most waves up to p's, then p's depth.  Returns false if none.
+inline bool mfma_ring_plan(MfmaPlan& p, int min_wpr, int N)
+{
+    const int sets = N / 16;
+    MfmaPlan best{};
+    int best_score = -1;
+#define SPK_RING(RT, CS, KW, D, PRE)                                                                 \
+    if (!PRE && RT == p.rt && KW <= min_wpr && sets % CS == 0) {                                    \
+        const int score = (CS == p.cs ? 1 << 20 : 0) + (KW <= p.kw ? KW << 8 : 0) + (D == p.d ? 1 : 0); \
+        if (score > best_score) {                                                                    \
+            best_score = score;                                                                      \
+            best = MfmaPlan{RT, CS, KW, D, false};                                                   \
+        }                                                                                            \
+    }
+    SPK_MFMA_PLANS(SPK_RING)
+#undef SPK_RING
+    if (best_score < 0)
+        return false;
+    p = best;
+    return true;
+}
+
 // Plan code reported by the library: rt | cs << 4 | kw << 8 | d << 16 | preload << 24.
 inline int mfma_plan_code(const MfmaPlan& p)
 {
@@ -451,6 +517,32 @@ hipError_t launch_mfma_t(const int8_t* P, const float* scale, int K, int N, cons
         hipLaunchKernelGGL((k_mfma<RT, CS, KW, D, PRELOAD, false>), dim3((unsigned)units), dim3(64 * KW), lds, st,
                            P, scale, N, mask, wpr, B, n_rowtiles, n_coltiles, out, acc);
     return hipGetLastError();
+}
+
+template <int RT, int CS, int KW, int D>
+hipError_t launch_mfma_items_t(const MfmaItems& items, int n_items, int max_wpr, int N, const uint64_t* mask, int B,
+                               float* out, hipStream_t st)
+{
+    const int n_coltiles = N / (16 * CS);
+    const int n_rowtiles = (B + 16 * RT - 1) / (16 * RT);
+    const int64_t units = (int64_t)n_coltiles * n_rowtiles * n_items;
+    if (units > 0x7fffffff)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_mfma_items<RT, CS, KW, D>), dim3((unsigned)units), dim3(64 * KW),
+                       mfma_lds_bytes(RT, CS, max_wpr), st, items, N, mask, B, n_rowtiles, n_coltiles, out);
+    return hipGetLastError();
+}
+
+// Launch of several projections for a ring plan (p.preload must be false).
+inline hipError_t launch_mfma_items(const MfmaPlan& p, const MfmaItems& items, int n_items, int max_wpr, int N,
+                                    const uint64_t* mask, int B, float* out, hipStream_t st)
+{
+#define SPK_LAUNCH_ITEMS(RT, CS, KW, D, PRE)                                                       \
+    if (!PRE && p.rt == RT && p.cs == CS && p.kw == KW && p.d == D && !p.preload)              \
+        return launch_mfma_items_t<RT, CS, KW, D>(items, n_items, max_wpr, N, mask, B, out, st);
+    SPK_MFMA_PLANS(SPK_LAUNCH_ITEMS)
+#undef SPK_LAUNCH_ITEMS
+    return hipErrorInvalidValue;
 }
 
 // Codes of every instantiated plan (host memory, up to cap); returns the count.

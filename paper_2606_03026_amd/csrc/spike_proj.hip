@@ -763,6 +763,83 @@ int spike_stack_forward(const spike_proj_t* projs, int32_t n_proj, const uint64_
     return SPIKE_OK;
 }
 
+int spike_stack_forward_fused(const spike_proj_t* projs, int32_t n_proj, const uint64_t* masks, int32_t B,
+                              float* out, void* stream)
+{
+    g_last_error.clear();
+    if (!projs || n_proj < 1)
+        return fail(SPIKE_EINVAL, "need at least one projection");
+    if (n_proj > spk::kMfmaMaxItems)
+        return fail(SPIKE_EUNSUPPORTED, "a fused launch holds at most %d projections", spk::kMfmaMaxItems);
+    if (B < 0)
+        return fail(SPIKE_EINVAL, "B = %d < 0", B);
+    for (int j = 0; j < n_proj; ++j) {
+        if (!projs[j])
+            return fail(SPIKE_EINVAL, "projection %d is null", j);
+        if (B > projs[j]->max_B)
+            return fail(SPIKE_EINVAL, "B = %d exceeds projection %d's reserved %d rows", B, j, projs[j]->max_B);
+    }
+    if (B == 0)
+        return SPIKE_OK;
+    if (!masks || !out)
+        return fail(SPIKE_EINVAL, "null mask or output pointer");
+    const int32_t N = projs[0]->N;
+    int32_t min_K = projs[0]->K;
+    int max_wpr = 0;
+    for (int j = 0; j < n_proj; ++j) {
+        if (projs[j]->N != N)
+            return fail(SPIKE_EUNSUPPORTED, "all projections of a fused launch must share N (%d vs %d)", projs[j]->N, N);
+        if (projs[j]->device != projs[0]->device)
+            return fail(SPIKE_EINVAL, "projections live on different devices");
+        min_K = std::min(min_K, projs[j]->K);
+        max_wpr = std::max(max_wpr, projs[j]->wpr);
+    }
+    if (int rc = check_device(projs[0]->device))
+        return rc;
+    // one ring plan for all items, chosen for the shortest K (every wave needs a k-step)
+    // Tiles of up to 64 rows by 48 channels, 16 waves, two k-steps in flight
+    // per wave (measured best on the 64-row decode stack: 1408 workgroups
+    // over 44 projections); the first handle's matrix-core tuning knobs
+    // override it for the whole launch.
+    const spike_proj* h0 = projs[0];
+    const int sets = N / spk::kMfmaNAlign;
+    spk::MfmaPlan p{};
+    p.rt = B <= 16 ? 1 : B <= 32 ? 2 : 4;
+    p.cs = sets % 3 == 0 ? 3 : sets % 2 == 0 ? 2 : 1;
+    p.kw = 16;
+    p.d = 2;
+    if (h0->mfma_row_tile > 0)
+        p.rt = h0->mfma_row_tile;
+    if (h0->mfma_col_sets > 0)
+        p.cs = h0->mfma_col_sets;
+    if (h0->mfma_waves > 0)
+        p.kw = h0->mfma_waves;
+    if (h0->mfma_depth > 0)
+        p.d = h0->mfma_depth;
+    if (N % spk::kMfmaNAlign != 0 || !spk::mfma_ring_plan(p, (int)words_per_row(min_K), N))
+        return fail(SPIKE_EUNSUPPORTED, "no matrix-core plan serves N = %d, K >= %d, B = %d in one launch", N, min_K, B);
+    spk::MfmaItems items{};
+    int64_t moff = 0, ooff = 0;
+    for (int j = 0; j < n_proj; ++j) {
+        const spike_proj* h = projs[j];
+        if (const char* why = mfma_refusal(h->K, N, h->packed != nullptr, B, p))
+            return fail(SPIKE_EUNSUPPORTED, "projection %d (K = %d) cannot run on the matrix cores with B = %d: %s", j,
+                        h->K, B, why);
+        items.P[j] = h->packed;
+        items.scale[j] = h->scale;
+        items.mask_off[j] = moff;
+        items.out_off[j] = ooff;
+        items.wpr[j] = h->wpr;
+        moff += (int64_t)B * h->wpr;
+        ooff += (int64_t)B * N;
+    }
+    if (spk::mfma_lds_bytes(p.rt, p.cs, max_wpr) > spk::kMfmaMaxLds)
+        return fail(SPIKE_EUNSUPPORTED, "the staged spike words of the longest projection exceed the LDS budget");
+    const hipError_t e = spk::launch_mfma_items(p, items, n_proj, max_wpr, N, masks, B, out,
+                                                static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SPIKE_OK : hip_fail(e, "fused matrix-core launch");
+}
+
 int spike_stream_create(const spike_proj_t* projs, int32_t n_proj, int32_t n_sets, int32_t n_tokens,
                         spike_stream_t* out_stream)
 {

@@ -226,18 +226,26 @@ def test_prefill_batch(sp):
         assert_parity(sp, h, d["W"], d["scale"], d["masks"])
 
 
-def test_batched_decode_stack(sp):
-    """B = 64 rows through all 44 projections, structured spikes, two steps."""
-    hs, host, masks_by_step = [], [], []
+@pytest.fixture(scope="module")
+def batched_stack(sp):
+    hs, host = [], []
     for (l, j) in wl.stack_order():
         W, s = wl.batched_stack_projection(l, j)
         hs.append(make(sp, W, s)[0])
         host.append((W, s))
     bits = [wl.batched_stack_bits(l, j, B=64, n_steps=2) for (l, j) in wl.stack_order()]
+    return hs, host, bits
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_batched_decode_stack(sp, batched_stack, fused):
+    """B = 64 rows through all 44 projections, structured spikes, two steps:
+    in stream order (one launch per projection) and fused (one launch)."""
+    hs, host, bits = batched_stack
     for step in range(2):
         masks = np.concatenate([wl.pack_bits(b[step]).reshape(-1) for b in bits])
         out = torch.full((sum(64 * h.N for h in hs),), float("nan"), device="cuda")
-        sp.spike_stack_forward(hs, dmask(masks), 64, out)
+        (sp.spike_stack_forward_fused if fused else sp.spike_stack_forward)(hs, dmask(masks), 64, out)
         torch.cuda.synchronize()
         got = out.cpu().numpy()
         ooff = 0
@@ -245,6 +253,53 @@ def test_batched_decode_stack(sp):
             ref = oracle.spike_forward(W, s, wl.pack_bits(b[step]), threads=8)
             np.testing.assert_array_equal(bits32(got[ooff:ooff + ref.size]), bits32(ref.reshape(-1)))
             ooff += ref.size
+
+
+@pytest.mark.parametrize("B", [5, 17, 64, 130])
+def test_fused_stack_ragged(sp, B):
+    """Fused launch over projections of different K (ragged K and B, junk
+    padding bits past K) against the oracle, and against the in-order driver."""
+    shapes = [(100, 96), (1536, 96), (70, 96), (4097, 96)]
+    hs, host, ms = [], [], []
+    for i, (K, N) in enumerate(shapes):
+        p = wl.small_problem(K, N, B, 0.2, seed=100 + i)
+        m = p["masks"].copy()
+        if K % 64:
+            m[:, -1] |= np.uint64(~((1 << (K % 64)) - 1) & 0xFFFFFFFFFFFFFFFF)  # junk past K
+        hs.append(make(sp, p["W"], p["scale"])[0])
+        host.append((p["W"], p["scale"]))
+        ms.append(m)
+    masks = np.concatenate([m.reshape(-1) for m in ms])
+    n_out = sum(B * N for _, N in shapes)
+    out_f = torch.full((n_out,), float("nan"), device="cuda")
+    out_s = torch.full((n_out,), float("nan"), device="cuda")
+    sp.spike_stack_forward_fused(hs, dmask(masks), B, out_f)
+    sp.spike_stack_forward(hs, dmask(masks), B, out_s)
+    torch.cuda.synchronize()
+    got = out_f.cpu().numpy()
+    assert np.array_equal(bits32(got), bits32(out_s.cpu().numpy()))
+    ooff = 0
+    for (W, s), m in zip(host, ms):
+        ref = oracle.spike_forward(W, s, m, threads=8)
+        np.testing.assert_array_equal(bits32(got[ooff:ooff + ref.size]), bits32(ref.reshape(-1)))
+        ooff += ref.size
+
+
+def test_fused_stack_refusals(sp):
+    """The fused launch refuses what it cannot run, before any launch."""
+    a = wl.small_problem(128, 64, 8, 0.2, seed=1)
+    b = wl.small_problem(128, 32, 8, 0.2, seed=2)
+    ha, hb = make(sp, a["W"], a["scale"])[0], make(sp, b["W"], b["scale"])[0]
+    out = torch.empty(8 * 96, device="cuda")
+    masks = dmask(np.concatenate([a["masks"].reshape(-1), b["masks"].reshape(-1)]))
+    with pytest.raises(sp.SpikeError) as ei:
+        sp.spike_stack_forward_fused([ha, hb], masks, 8, out)  # different N
+    assert ei.value.code == sp.SPIKE_EUNSUPPORTED
+    c = wl.small_problem(128, 64, 8, 0.2, seed=3)
+    hc = sp.spike_proj_create_reserved(dev(c["W"]), dev(c["scale"]), 4)  # no matrix-core copy
+    with pytest.raises(sp.SpikeError) as ei:
+        sp.spike_stack_forward_fused([ha, hc], masks, 4, out)
+    assert ei.value.code == sp.SPIKE_EUNSUPPORTED
 
 
 def test_batch_zero_is_a_noop(sp):
