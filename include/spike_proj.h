@@ -75,33 +75,38 @@ int spike_proj_create(const int8_t *W_int8_colmajor, const float *scale_fp32, in
                       spike_proj_t *out_handle);
 
 /* spike_proj_create with the workspace sized for max_B rows (1 <= max_B <=
- * 65535) instead of SPIKE_DEFAULT_MAX_B.  Below the matrix-core minimum
- * batch (SPIKE_TUNE_MFMA_MIN_B, default 5) no matrix-core copy of W is made:
- * handles meant for batch-1 calls or streams then hold only a workspace of
- * max_B * N INT32 entries and never a second copy of the weights. */
+ * 65535) instead of SPIKE_DEFAULT_MAX_B.  flags: 0, or
+ * SPIKE_CREATE_GATHER_ONLY for a handle that never holds the matrix-core
+ * copy of W (every call then runs the active-column gather, and the handle
+ * holds only a workspace of max_B * N INT32 entries: handles meant for
+ * streams of batch-1 projections, or many address-distinct copies of
+ * weights).  Unknown flags: SPIKE_EINVAL. */
+#define SPIKE_CREATE_GATHER_ONLY 1
 int spike_proj_create_reserved(const int8_t *W_int8_colmajor, const float *scale_fp32, int32_t K, int32_t N,
-                               int32_t max_B, spike_proj_t *out_handle);
+                               int32_t max_B, int32_t flags, spike_proj_t *out_handle);
 
 /* Resize the workspace so that forward() accepts up to max_B rows
  * (1 <= max_B <= 65535).  A max_B below the matrix-core minimum batch
- * (SPIKE_TUNE_MFMA_MIN_B, default 5) also frees the matrix-core copy of W,
- * so handles that only ever run batch-1 calls hold no second copy; a larger
- * max_B makes the copy again where the shape allows it.  Allocates and
+ * (SPIKE_TUNE_MFMA_MIN_B, default 1) also frees the matrix-core copy of W;
+ * a max_B at or above it makes the copy again where the shape allows it
+ * (never for a SPIKE_CREATE_GATHER_ONLY handle).  Allocates and
  * synchronises the device; call it outside graph capture and while no
  * forward() of this handle is in flight. */
 int spike_proj_reserve(spike_proj_t h, int32_t max_B);
 
 /* y = Eq. (sparse) for B spike rows: out[b*N + n].  Asynchronous on
  * `stream` (a hipStream_t; NULL means the default stream).  B = 0 is a
- * no-op; 0 <= B <= the reserved max_B.  Dispatches to the active-column
- * gather (decode-sized B) or to the dense i8 matrix-core contraction over
- * the 0/1 spike matrix (batches from SPIKE_TUNE_MFMA_MIN_B rows, where the
- * handle has the matrix-core copy of W and the matrix-core launch plan can
- * run; otherwise the gather serves the call); both give identical bits.
- * With SPIKE_PATH_MFMA forced where the matrix-core plan cannot run (no
- * copy of W, a tuned plan that is not instantiated or does not fit, more
- * rows than 31-bit offsets into the mask can address) it returns
- * SPIKE_EUNSUPPORTED. */
+ * no-op; 0 <= B <= the reserved max_B.  Dispatches to the dense i8
+ * matrix-core contraction over the 0/1 spike matrix (every product is 0 or
+ * a weight, so the sum is the same active-column sum) wherever the handle
+ * has the matrix-core copy of W and a matrix-core launch plan can run, from
+ * SPIKE_TUNE_MFMA_MIN_B rows (default 1: measured faster than the gather
+ * per call at every batch up to 64 and every spike rate from 0.02 to 0.40
+ * on the 1536- and 6144-input shapes, since one call is latency-bound);
+ * otherwise to the active-column gather.  Both give identical bits.  With
+ * SPIKE_PATH_MFMA forced where the matrix-core plan cannot run (no copy of
+ * W, a tuned plan that is not instantiated or does not fit, more rows than
+ * 31-bit offsets into the mask can address) it returns SPIKE_EUNSUPPORTED. */
 int spike_proj_forward(spike_proj_t h, const uint64_t *spike_bitmask, int32_t B, float *out_fp32,
                        void *stream);
 
@@ -142,6 +147,7 @@ int spike_proj_destroy(spike_proj_t h);
  *   SPIKE_TUNE_SLICE_WORDS  64-bit mask words per K-slice of the gather
  *                           (0 = automatic; 1..256)
  *   SPIKE_TUNE_MFMA_MIN_B   smallest B sent to the matrix-core path by AUTO
+ *                           (default 1)
  *   SPIKE_TUNE_VEC          bytes per lane per column load of the gather:
  *                           0 = automatic, 1, 4, 8 or 16 (16, 8 and 4 need
  *                           N and the W address to be multiples of it)

@@ -43,7 +43,7 @@ _lib = ctypes.CDLL(LIB)
 _p, _i32 = ctypes.c_void_p, ctypes.c_int32
 _sig = {
     "spike_proj_create": [_p, _p, _i32, _i32, ctypes.POINTER(_p)],
-    "spike_proj_create_reserved": [_p, _p, _i32, _i32, _i32, ctypes.POINTER(_p)],
+    "spike_proj_create_reserved": [_p, _p, _i32, _i32, _i32, _i32, ctypes.POINTER(_p)],
     "spike_proj_reserve": [_p, _i32],
     "spike_proj_forward": [_p, _p, _i32, _p, _p],
     "spike_proj_forward_acc": [_p, _p, _i32, _p, _p],
@@ -137,12 +137,16 @@ def spike_proj_create(W: torch.Tensor, scale: torch.Tensor) -> SpikeProj:
     return SpikeProj(out.value, W, scale)
 
 
-def spike_proj_create_reserved(W: torch.Tensor, scale: torch.Tensor, max_B: int) -> SpikeProj:
-    """spike_proj_create with a workspace for max_B rows (no matrix-core copy below the minimum batch)."""
+SPIKE_CREATE_GATHER_ONLY = 1
+
+
+def spike_proj_create_reserved(W: torch.Tensor, scale: torch.Tensor, max_B: int, gather_only: bool = False) -> SpikeProj:
+    """spike_proj_create with a workspace for max_B rows; gather_only: never hold the matrix-core copy."""
     _check_operands(W, scale)
     out = _p()
     _check(_lib.spike_proj_create_reserved(_dev_ptr(W, "W"), _dev_ptr(scale, "scale"), W.shape[0], W.shape[1],
-                                           int(max_B), ctypes.byref(out)), "spike_proj_create_reserved")
+                                           int(max_B), SPIKE_CREATE_GATHER_ONLY if gather_only else 0,
+                                           ctypes.byref(out)), "spike_proj_create_reserved")
     h = SpikeProj(out.value, W, scale)
     h.max_B = int(max_B)
     return h

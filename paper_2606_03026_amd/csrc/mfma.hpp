@@ -417,7 +417,14 @@ inline MfmaPlan mfma_plan(int K, int N, int B, int rt_req, int cs_req, int kw_re
     const int wpr = (K + 63) / 64;
     const int sets = N / 16;
     MfmaPlan p{};
-    if (B <= 64) {
+    if (B <= 16) {
+        // one row tile: one channel set per workgroup (the most workgroups),
+        // 8 waves for short K, 16 for long K (measured per dependent call on
+        // the 1536- and 6144-input shapes)
+        p.rt = 1;
+        p.cs = 1;
+        p.kw = wpr <= 32 ? 8 : 16;
+    } else if (B <= 64) {
         // measured on the 64-row decode stack: two channel sets, 8 waves
         p.rt = 1;
         p.cs = sets % 2 == 0 ? 2 : 1;
@@ -443,6 +450,8 @@ inline MfmaPlan mfma_plan(int K, int N, int B, int rt_req, int cs_req, int kw_re
     const int steps = (wpr + p.kw - 1) / p.kw;
     if (d_req > 0)
         p.d = d_req;
+    else if (B <= 16)
+        p.d = wpr <= 32 ? 4 : 2;  // short K: every step preloaded; long K: a ring of 2
     else if (B <= 64)
         p.d = 4;  // preloads up to 4 steps per wave, a ring of 4 beyond
     else if (wpr < 32)
@@ -469,17 +478,19 @@ inline MfmaPlan mfma_plan(int K, int N, int B, int rt_req, int cs_req, int kw_re
 }
 
 // A ring plan (any k-step count) for a launch whose projections all have
-// at least min_wpr k-steps: the instantiated ring plan with p's row tile
-// and a channel-set count dividing N / 16, preferring p's channel sets,
-// then the most waves up to p's, then p's depth.  Returns false if none.
+// at least min_wpr k-steps: an instantiated ring plan with a channel-set
+// count dividing N / 16 and at most min_wpr waves, preferring p's row tile,
+// then p's channel sets, then the most waves up to p's, then p's depth.
+// Returns false if none.
 inline bool mfma_ring_plan(MfmaPlan& p, int min_wpr, int N)
 {
     const int sets = N / 16;
     MfmaPlan best{};
     int best_score = -1;
 #define SPK_RING(RT, CS, KW, D, PRE)                                                                 \
-    if (!PRE && RT == p.rt && KW <= min_wpr && sets % CS == 0) {                                    \
-        const int score = (CS == p.cs ? 1 << 20 : 0) + (KW <= p.kw ? KW << 8 : 0) + (D == p.d ? 1 : 0); \
+    if (!PRE && KW <= min_wpr && sets % CS == 0) {                                                  \
+        const int score = (RT == p.rt ? 1 << 24 : 0) + (CS == p.cs ? 1 << 20 : 0) +                 \
+                          (KW <= p.kw ? KW << 8 : 0) + (D == p.d ? 1 : 0);                          \
         if (score > best_score) {                                                                    \
             best_score = score;                                                                      \
             best = MfmaPlan{RT, CS, KW, D, false};                                                   \

@@ -150,8 +150,13 @@ constexpr int kLatencySliceWords = 24;
 
 constexpr int kMinTile = 32;  // smallest tile of any shape: sizes the counter array
 
-// Smallest batch that AUTO sends to the matrix cores.
-constexpr int kDefaultMfmaMinB = 5;
+// Smallest batch that AUTO sends to the matrix cores: every batch.  Measured
+// per dependent call on the 1536 -> 1536 and 6144 -> 1536 shapes, the dense
+// contraction is faster than the gather at every B up to 64 and every
+// density from 0.02 to 0.40 (a batch-1 call is latency-bound: reading all of
+// W at HBM rate costs less than the gather's compaction and K-split
+// hand-off).
+constexpr int kDefaultMfmaMinB = 1;
 
 }  // namespace
 
@@ -165,6 +170,7 @@ struct spike_proj {
     uint32_t* counters = nullptr;  // [max_B][counter_stride], zero between calls
     int32_t counter_stride = 0;
     int8_t* packed = nullptr;      // matrix-core operand copy of W (null: no matrix-core path)
+    bool gather_only = false;      // created with SPIKE_CREATE_GATHER_ONLY: never holds the copy
     int path = SPIKE_PATH_AUTO;
     int slice_words = 0;  // 0 = automatic
     int max_slices = 16;
@@ -497,7 +503,7 @@ int static_scratch(int dev, hipStream_t st, uint32_t** out)
 extern "C" {
 
 int spike_proj_create_reserved(const int8_t* W, const float* scale, int32_t K, int32_t N, int32_t max_B,
-                               spike_proj_t* out_handle)
+                               int32_t flags, spike_proj_t* out_handle)
 {
     g_last_error.clear();
     if (!out_handle)
@@ -511,6 +517,8 @@ int spike_proj_create_reserved(const int8_t* W, const float* scale, int32_t K, i
         return fail(SPIKE_EINVAL, "N = %d outside [1, %d]", N, SPIKE_MAX_N);
     if (max_B < 1 || max_B > 65535)
         return fail(SPIKE_EINVAL, "max_B = %d outside [1, 65535]", max_B);
+    if (flags & ~SPIKE_CREATE_GATHER_ONLY)
+        return fail(SPIKE_EINVAL, "unknown create flags 0x%x", flags);
     spike_proj* h = new (std::nothrow) spike_proj;
     if (!h)
         return fail(SPIKE_ENOMEM, "handle allocation failed");
@@ -520,6 +528,7 @@ int spike_proj_create_reserved(const int8_t* W, const float* scale, int32_t K, i
     h->N = N;
     h->wpr = (int32_t)words_per_row(K);
     h->shape = default_shape(W, N, 0);
+    h->gather_only = (flags & SPIKE_CREATE_GATHER_ONLY) != 0;
     hipError_t e = hipGetDevice(&h->device);
     if (e != hipSuccess) {
         delete h;
@@ -530,7 +539,7 @@ int spike_proj_create_reserved(const int8_t* W, const float* scale, int32_t K, i
         return rc;
     }
     // the matrix-core copy of W only where batches that use it can be run
-    if (max_B >= h->mfma_min_b) {
+    if (!h->gather_only && max_B >= h->mfma_min_b) {
         if (int rc = make_packed(h)) {
             (void)hipFree(h->ws);
             (void)hipFree(h->counters);
@@ -544,7 +553,7 @@ int spike_proj_create_reserved(const int8_t* W, const float* scale, int32_t K, i
 
 int spike_proj_create(const int8_t* W, const float* scale, int32_t K, int32_t N, spike_proj_t* out_handle)
 {
-    return spike_proj_create_reserved(W, scale, K, N, SPIKE_DEFAULT_MAX_B, out_handle);
+    return spike_proj_create_reserved(W, scale, K, N, SPIKE_DEFAULT_MAX_B, 0, out_handle);
 }
 
 int spike_proj_reserve(spike_proj_t h, int32_t max_B)
@@ -554,7 +563,8 @@ int spike_proj_reserve(spike_proj_t h, int32_t max_B)
         return fail(SPIKE_EINVAL, "null handle");
     if (max_B < 1 || max_B > 65535)
         return fail(SPIKE_EINVAL, "max_B = %d outside [1, 65535]", max_B);
-    if (max_B == h->max_B && (max_B < h->mfma_min_b || h->packed || !spk::mfma_supported(h->K, h->N)))
+    if (max_B == h->max_B &&
+        (h->gather_only || max_B < h->mfma_min_b || h->packed || !spk::mfma_supported(h->K, h->N)))
         return SPIKE_OK;
     if (int rc = check_device(h->device))
         return rc;
@@ -565,7 +575,7 @@ int spike_proj_reserve(spike_proj_t h, int32_t max_B)
         return rc;
     // The matrix-core copy of W is kept only while batches that would use it
     // can be run: fewer reserved rows than the matrix-core minimum free it.
-    if (max_B < h->mfma_min_b) {
+    if (h->gather_only || max_B < h->mfma_min_b) {
         if (h->packed)
             (void)hipFree(h->packed);
         h->packed = nullptr;

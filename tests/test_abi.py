@@ -84,19 +84,37 @@ def test_automatic_matrix_core_plans_are_instantiated(sp):
     cores, the plan is one the library instantiates; the decode shapes and
     the prefill shape go where the design puts them (no GPU needed)."""
     plans = {tuple(p.values()) for p in sp.spike_mfma_plans()}
-    for K in (1, 63, 64, 65, 100, 1000, 1536, 2048, 4097, 6144, 16384, 20000, 40000):
+    for K in (1, 63, 64, 65, 100, 300, 1000, 1536, 2048, 4097, 6144, 16384, 20000, 40000):
         for N in (16, 64, 100, 192, 1536, 6144, 1 << 20):
-            for B in (1, 4, 5, 17, 64, 65, 130, 512, 4096):
+            for B in (1, 4, 5, 16, 17, 64, 65, 130, 512, 4096):
                 path, plan = sp.spike_proj_plan_query(K, N, B)
                 if path == sp.SPIKE_PATH_MFMA:
                     assert tuple(plan.values()) in plans, (K, N, B, plan)
-                    assert B >= 5 and N % 16 == 0
+                    assert N % 16 == 0
                 else:
                     assert path == sp.SPIKE_PATH_GATHER
-    assert sp.spike_proj_plan_query(1536, 1536, 1)[0] == sp.SPIKE_PATH_GATHER
-    assert sp.spike_proj_plan_query(6144, 1536, 4)[0] == sp.SPIKE_PATH_GATHER
+                    # the gather serves what the matrix cores cannot: N not a
+                    # multiple of 16, a packed copy of 2^31 bytes or more, or
+                    # rows whose staged spike words (16 rows of ceil(K/64) | 1
+                    # words) do not fit the 64 KB LDS budget
+                    staged = 16 * (((K + 63) // 64) | 1) * 8
+                    assert N % 16 != 0 or (K + 63) // 64 * 64 * N >= 1 << 31 or staged > 60000, (K, N, B)
+    # batch-1 decode calls and small batches: one channel set per workgroup
     for K in (1536, 6144):
+        for B in (1, 4, 16):
+            path, plan = sp.spike_proj_plan_query(K, 1536, B)
+            assert path == sp.SPIKE_PATH_MFMA and plan["rt"] == 1 and plan["cs"] == 1
         path, plan = sp.spike_proj_plan_query(K, 1536, 64)
         assert path == sp.SPIKE_PATH_MFMA and plan["rt"] == 1
     path, plan = sp.spike_proj_plan_query(6144, 1536, 512)
     assert path == sp.SPIKE_PATH_MFMA and plan["rt"] == 4
+    assert sp.spike_proj_plan_query(1536, 1000, 1)[0] == sp.SPIKE_PATH_GATHER
+
+
+def test_create_rejects_unknown_flags(sp):
+    lib = sp.raw_library()
+    out = ctypes.c_void_p()
+    dummy = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    assert lib.spike_proj_create_reserved(dummy, dummy, 4, 4, 1, 2, ctypes.byref(out)) == sp.SPIKE_EINVAL
+    assert "flags" in sp.spike_proj_last_error()
+    assert lib.spike_proj_create_reserved(dummy, dummy, 4, 4, 0, 0, ctypes.byref(out)) == sp.SPIKE_EINVAL

@@ -110,10 +110,20 @@ def test_every_vector_width_on_the_decode_shape(sp, vec):
         assert_parity(sp, h, d["W"], d["scale"], d["masks"])
 
 
-def test_single_projection_batch1(sp):
-    """1536 -> 1536, Bernoulli(0.10): independent batch-1 calls, then one batch."""
+PATHS = ["auto", "gather"]
+
+
+def set_path(sp, h, path):
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_GATHER if path == "gather" else sp.SPIKE_PATH_AUTO)
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_single_projection_batch1(sp, path):
+    """1536 -> 1536, Bernoulli(0.10): independent batch-1 calls, then one
+    batch; on the automatic path (matrix cores) and on the gather."""
     d = wl.single_projection(n_masks=32)
     h, *_ = make(sp, d["W"], d["scale"])
+    set_path(sp, h, path)
     ref = oracle.spike_forward(d["W"], d["scale"], d["masks"])
     for i in range(32):
         got = gpu_forward(sp, h, d["masks"][i:i + 1])
@@ -121,10 +131,12 @@ def test_single_projection_batch1(sp):
     assert_parity(sp, h, d["W"], d["scale"], d["masks"])
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("p", wl.DOWN_SWEEP_RATES)
-def test_down_projection_sweep(sp, p):
+def test_down_projection_sweep(sp, p, path):
     d = wl.down_sweep(p, n_masks=8)
     h, *_ = make(sp, d["W"], d["scale"])
+    set_path(sp, h, path)
     ref = oracle.spike_forward(d["W"], d["scale"], d["masks"])
     for i in range(8):
         np.testing.assert_array_equal(bits32(gpu_forward(sp, h, d["masks"][i:i + 1])), bits32(ref[i:i + 1]))
@@ -143,8 +155,11 @@ def stack(sp):
     return hs, host
 
 
-def test_stack_driver_in_order(sp, stack):
+@pytest.mark.parametrize("path", PATHS)
+def test_stack_driver_in_order(sp, stack, path):
     hs, host = stack
+    for h in hs:
+        set_path(sp, h, path)
     T = 3
     masks = wl.stack_token_masks(T)
     per_tok_out = sum(h.N for h in hs)
@@ -160,6 +175,8 @@ def test_stack_driver_in_order(sp, stack):
             np.testing.assert_array_equal(bits32(got[ooff:ooff + h.N]), bits32(ref))
             moff += wpr
             ooff += h.N
+    for h in hs:
+        set_path(sp, h, "auto")
 
 
 @pytest.mark.parametrize("n_sets", [1, 2])
@@ -296,7 +313,7 @@ def test_fused_stack_refusals(sp):
         sp.spike_stack_forward_fused([ha, hb], masks, 8, out)  # different N
     assert ei.value.code == sp.SPIKE_EUNSUPPORTED
     c = wl.small_problem(128, 64, 8, 0.2, seed=3)
-    hc = sp.spike_proj_create_reserved(dev(c["W"]), dev(c["scale"]), 4)  # no matrix-core copy
+    hc = sp.spike_proj_create_reserved(dev(c["W"]), dev(c["scale"]), 4, gather_only=True)  # no matrix-core copy
     with pytest.raises(sp.SpikeError) as ei:
         sp.spike_stack_forward_fused([ha, hc], masks, 4, out)
     assert ei.value.code == sp.SPIKE_EUNSUPPORTED
@@ -367,6 +384,7 @@ def test_maximum_K(sp, case):
 def test_repeat_runs_are_bit_identical(sp):
     d = wl.down_sweep(0.2, n_masks=4)
     h, *_ = make(sp, d["W"], d["scale"])
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_GATHER)
     ref = None
     for sw in (0, 1, 2, 7, 96):
         sp.spike_proj_tune(h, sp.SPIKE_TUNE_SLICE_WORDS, sw)
@@ -409,11 +427,13 @@ def test_row_major_weights_fail_parity(sp):
     assert (bits32(got) != bits32(ref)).any()
 
 
-def test_side_stream_and_graph_replay(sp):
+@pytest.mark.parametrize("path", PATHS)
+def test_side_stream_and_graph_replay(sp, path):
     hs, host = [], []
     for K in (1536, 6144, 1536):
         p = wl.small_problem(K, 1536, 1, 0.1, seed=K)
         hs.append(make(sp, p["W"], p["scale"])[0])
+        set_path(sp, hs[-1], path)
         host.append((p["W"], p["scale"]))
     words = sum(wl.words_per_row(h.K) for h in hs)
     static_mask = torch.zeros(words, dtype=torch.int64, device="cuda")
@@ -647,11 +667,12 @@ def test_auto_falls_back_when_the_plan_cannot_run(sp):
 
 
 def test_reserve_drops_and_remakes_the_matrix_core_copy(sp):
-    """reserve() below the matrix-core minimum frees the packed copy (the
-    matrix cores then refuse, AUTO uses the gather); a larger reserve makes it
-    again from W."""
+    """With the matrix-core minimum raised to 5 rows, reserve() below it
+    frees the packed copy (the matrix cores then refuse, AUTO uses the
+    gather); a larger reserve makes it again from W."""
     p = wl.small_problem(1000, 256, 20, 0.2, seed=5)
     h, *_ = make(sp, p["W"], p["scale"])
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_MFMA_MIN_B, 5)
     sp.spike_proj_reserve(h, 1)
     sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_MFMA)
     out = torch.empty((1, 256), device="cuda")
