@@ -315,6 +315,37 @@ def bench_batched_stack(sp, torch, wl, timer, steps: int = 16, B: int = 64):
     return r
 
 
+def crossover_sweep(sp, torch, timer):
+    """Per-call time of the gather and of the matrix cores over K in {1536,
+    6144}, spike rate p and batch B (N = 1536): each cell is 20 dependent
+    calls captured in one graph, replayed 5 times.  Prints one JSON row per
+    cell; the data behind the automatic path choice."""
+    from paper_2606_03026_amd import workloads as wl
+    rows = []
+    for K in (1536, 6144):
+        N = 1536
+        rng = np.random.default_rng([42, 7, K])
+        W = rng.integers(-127, 127, size=(K, N), dtype=np.int8, endpoint=True)
+        s = rng.uniform(1e-3, 1e-2, N).astype(np.float32)
+        h = make_handles(sp, torch, [(W, s)], 1, max_B=512)[0][0]
+        for p in (0.02, 0.05, 0.10, 0.20, 0.40):
+            for B in (1, 2, 3, 4, 5, 6, 8, 12, 16, 24, 32, 64, 128, 256, 512):
+                bits = rng.random((B, K)) < p
+                dm = torch.from_numpy(wl.pack_bits(bits).view(np.int64)).cuda()
+                out = torch.empty((B, N), device="cuda")
+                t = {}
+                for name, path in (("gather", sp.SPIKE_PATH_GATHER), ("mfma", sp.SPIKE_PATH_MFMA)):
+                    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, path)
+                    g = graph_of(torch, lambda: [sp.spike_proj_forward(h, dm, B, out) for _ in range(20)])
+                    t[name] = timer(g.replay, 5, 1) / 20
+                    del g
+                rows.append({"K": K, "N": N, "p": p, "B": B, "gather_us": round(t["gather"] * 1e6, 2),
+                             "mfma_us": round(t["mfma"] * 1e6, 2)})
+                print(json.dumps(rows[-1]), flush=True)
+        h.close()
+    return rows
+
+
 def traffic_record():
     """HBM bytes per stream launch from the committed rocprofv3 PMC summary,
     if it was taken on the current kernel sources."""
@@ -340,6 +371,10 @@ def main(argv=None) -> int:
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-latency", action="store_true")
     ap.add_argument("--only-stream", action="store_true", help="time only the headline stream (for profiling)")
+    ap.add_argument("--crossover", action="store_true",
+                    help="only the per-call gather vs matrix-core sweep over (K, p, B), one JSON row per cell")
+    ap.add_argument("--only-mfma", action="store_true",
+                    help="time only the matrix-core workloads, prefill and batched stack (for profiling)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a 1 GiB device copy first (reference for the PMC byte counters)")
     args = ap.parse_args(argv)
@@ -364,6 +399,14 @@ def main(argv=None) -> int:
         log("copy probe: 1 GiB read + 1 GiB written")
         del src, dst
 
+    if args.crossover:
+        crossover_sweep(sp, torch, timer)
+        return 0
+    if args.only_mfma:
+        res = {"prefill_512x6144x1536": bench_prefill(sp, torch, wl, timer),
+               "batched_stack_b64": bench_batched_stack(sp, torch, wl, timer)}
+        print(json.dumps({"workloads": res}), flush=True)
+        return 0
     if args.only_stream:
         args.no_latency = True
     main_res = bench_decode_stack(sp, torch, wl, timer, args)
