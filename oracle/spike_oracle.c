@@ -198,3 +198,38 @@ done:
     free(tids);
     return status;
 }
+
+/*
+ * Dense continuous-input projection (paper Sec. 2.3, last sentences of
+ * "Quantization and Accumulation"; Fig. "execution", lower path): weights of
+ * the continuous-input projections stay row-major, Q[m*K + k] = Q_{m,k}, one
+ * scale s_m per output channel.  Each INT8 weight is converted to a real
+ * number, multiplied by the FP32 activation x_k, the products of a row are
+ * summed, and the row scale is applied once:
+ *
+ *   y_m = s_m * sum_k Q_{m,k} * x_k
+ *
+ * The GPU accumulates in FP32 (the paper's precision); this oracle computes
+ * the same expression in float64, which is exact up to one rounding per
+ * addition at 2^-53, so comparisons use a tolerance derived from the GPU's
+ * FP32 summation tree.  x is B rows of K floats, y is B rows of M doubles.
+ */
+int oracle_dense_forward(const int8_t *Q, const float *scale, int64_t K, int64_t M, const float *x,
+                         int64_t B, double *y)
+{
+    if (K < 1 || M < 1 || B < 0)
+        return -1;
+    if (B > 0 && (!Q || !scale || !x || !y))
+        return -1;
+    for (int64_t b = 0; b < B; ++b) {
+        const float *xb = x + b * K;
+        for (int64_t m = 0; m < M; ++m) {
+            const int8_t *row = Q + m * K;
+            double dot = 0.0;
+            for (int64_t k = 0; k < K; ++k)
+                dot += (double)row[k] * (double)xb[k];
+            y[b * M + m] = (double)scale[m] * dot;
+        }
+    }
+    return 0;
+}

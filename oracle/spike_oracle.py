@@ -48,6 +48,8 @@ def load():
         lib.oracle_spike_acc.restype = ctypes.c_int
         lib.oracle_spike_forward.argtypes = [p, p, i64, i64, p, i64, p, ctypes.c_int]
         lib.oracle_spike_forward.restype = ctypes.c_int
+        lib.oracle_dense_forward.argtypes = [p, p, i64, i64, p, i64, p]
+        lib.oracle_dense_forward.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -100,3 +102,23 @@ def spike_forward(W: np.ndarray, scale: np.ndarray, mask: np.ndarray, threads: i
     if rc != 0:
         raise RuntimeError(f"oracle_spike_forward failed ({rc})")
     return out
+
+
+def dense_forward(Q: np.ndarray, scale: np.ndarray, x: np.ndarray) -> np.ndarray:
+    """Dense continuous-input projection, float64 [B, M]: y = scale[m] * sum_k Q[m, k] * x[b, k]
+    for row-major INT8 Q [M, K], FP32 scale [M] and FP32 x [B, K]."""
+    Q = np.ascontiguousarray(Q, dtype=np.int8)
+    M, K = Q.shape
+    scale = np.ascontiguousarray(scale, dtype=np.float32)
+    if scale.shape != (M,):
+        raise ValueError(f"scale must have one entry per output channel ({M}), got {scale.shape}")
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.ndim == 1:
+        x = x[None]
+    if x.shape[1] != K:
+        raise ValueError(f"x rows must hold K = {K} values, got {x.shape[1]}")
+    y = np.empty((x.shape[0], M), dtype=np.float64)
+    rc = load().oracle_dense_forward(_ptr(Q), _ptr(scale), K, M, _ptr(x), x.shape[0], _ptr(y))
+    if rc != 0:
+        raise RuntimeError(f"oracle_dense_forward failed ({rc})")
+    return y

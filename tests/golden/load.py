@@ -41,3 +41,33 @@ def load_hand_example(name: str = "hand_worked_example.txt"):
         acc=np.array(acc, dtype=np.int32),
         out_bits=np.array(out, dtype=np.uint32),
     )
+
+
+def load_dense_example(name: str = "dense_hand_example.txt"):
+    """The hand-worked dense projection example: Q [M, K] int8 row-major,
+    scale [M] f32, x [B, K] f32, y [B, M] f64 (exact)."""
+    Q, scale, x, y = [], None, [], []
+    M = K = None
+    with open(os.path.join(HERE, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            key, *vals = line.split()
+            if key == "M":
+                M = int(vals[0])
+            elif key == "K":
+                K = int(vals[0])
+            elif key == "Q":
+                Q.append([int(v) for v in vals])
+            elif key == "scale":
+                scale = np.array([float(v) for v in vals], dtype=np.float32)
+            elif key == "x":
+                x.append([float(v) for v in vals])
+            elif key == "y":
+                y.append([float(v) for v in vals])
+            else:
+                raise ValueError(f"unknown key {key}")
+    Q = np.array(Q, dtype=np.int8)
+    assert Q.shape == (M, K)
+    return dict(M=M, K=K, Q=Q, scale=scale, x=np.array(x, dtype=np.float32), y=np.array(y, dtype=np.float64))
