@@ -1,4 +1,5 @@
-"""ctypes binding of libspike_proj.so (C ABI in include/spike_proj.h).
+"""ctypes binding of libspike_proj.so (C ABI in include/spike_proj.h and
+include/dense_proj.h).
 
 Argument marshalling only: every step of the projection runs in the HIP
 kernels of the library.  Tensors are torch device tensors; their data
@@ -21,6 +22,9 @@ SPIKE_TUNE_MFMA_DEPTH, SPIKE_TUNE_MFMA_ROW_TILE, SPIKE_TUNE_MFMA_COL_SETS = 11, 
 SPIKE_SHAPE_NT = 1 << 25
 SPIKE_PATH_AUTO, SPIKE_PATH_GATHER, SPIKE_PATH_MFMA = 0, 1, 2
 SPIKE_DEFAULT_MAX_B = 512
+DENSE_MAX_K, DENSE_MAX_B = 16128, 65535
+DENSE_KERNEL_STAGED, DENSE_KERNEL_REGISTER = 1, 2
+DENSE_TUNE_KERNEL, DENSE_TUNE_WG_PER_CU = 1, 2
 
 
 def SPIKE_SHAPE(V: int, LG: int, U: int, BLOCK: int, NT: bool = False) -> int:
@@ -33,7 +37,7 @@ EXPORTED = (
     "spike_stream_create", "spike_stream_forward", "spike_stream_tune", "spike_stream_destroy",
     "spike_proj_last_error", "spike_proj_shapes", "spike_mfma_plans", "spike_proj_plan_query",
     "spike_proj_abi_version", "spike_proj_forward_noalloc", "spike_proj_create_reserved",
-    "spike_stack_forward_fused",
+    "spike_stack_forward_fused", "dense_proj_forward", "dense_proj_plan", "dense_proj_tune",
 )
 
 if not os.path.exists(LIB):
@@ -61,6 +65,9 @@ _sig = {
     "spike_proj_shapes": [_p, _i32],
     "spike_mfma_plans": [_p, _i32],
     "spike_proj_plan_query": [_i32, _i32, _i32, _p, _p],
+    "dense_proj_forward": [_p, _p, _i32, _i32, _p, _i32, _p, _p],
+    "dense_proj_plan": [_i32, _i32, _i32, _i32, _p, _p, _p, _p],
+    "dense_proj_tune": [_i32, _i32],
 }
 for _name, _args in _sig.items():
     getattr(_lib, _name).argtypes = _args
@@ -301,6 +308,34 @@ def spike_proj_plan_query(K: int, N: int, B: int):
     _check(_lib.spike_proj_plan_query(int(K), int(N), int(B), ctypes.byref(path), ctypes.byref(plan)),
            "spike_proj_plan_query")
     return path.value, (decode_plan(plan.value) if plan.value else None)
+
+
+def dense_proj_forward(Q: torch.Tensor, scale: torch.Tensor, x: torch.Tensor, B: int, y: torch.Tensor,
+                       stream=None) -> None:
+    """y[:B] = scale * (x[:B] @ float(Q).T) for row-major INT8 Q [M][K] (dense_proj.h)."""
+    if Q.dtype != torch.int8 or Q.dim() != 2:
+        raise TypeError("Q must be a 2-D int8 tensor [M][K]")
+    M, K = Q.shape
+    if scale.dtype != torch.float32 or scale.numel() != M:
+        raise TypeError("scale must be float32 with M entries")
+    if x.dtype != torch.float32 or y.dtype != torch.float32:
+        raise TypeError("x and y must be float32")
+    B = int(B)
+    _check(_lib.dense_proj_forward(_dev_ptr(Q, "Q"), _dev_ptr(scale, "scale"), int(K), int(M),
+                                   _dev_ptr(x, "x", B * K * 4), B, _dev_ptr(y, "y", B * M * 4), _stream(stream)),
+           "dense_proj_forward")
+
+
+def dense_proj_plan(K: int, M: int, B: int, q_align: int = 16) -> dict:
+    """Launch shape of the first launch dense_proj_forward makes (host-only)."""
+    out = [ctypes.c_int32() for _ in range(4)]
+    _check(_lib.dense_proj_plan(int(K), int(M), int(B), int(q_align), *[ctypes.byref(o) for o in out]),
+           "dense_proj_plan")
+    return dict(zip(("kernel", "vec", "rows_per_launch", "workgroups"), (o.value for o in out)))
+
+
+def dense_proj_tune(key: int, value: int) -> None:
+    _check(_lib.dense_proj_tune(int(key), int(value)), "dense_proj_tune")
 
 
 def spike_proj_abi_version() -> int:

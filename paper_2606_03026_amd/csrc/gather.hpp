@@ -31,6 +31,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "buffer.hpp"
+
 namespace spk {
 
 constexpr int kMaxSliceWords = 256;  // mask words per K-slice (16384 columns)
@@ -147,9 +149,6 @@ __device__ inline void wait_writes_done() { __builtin_amdgcn_s_waitcnt(0); }
 
 // V bytes of one column for one lane, added into V INT32 accumulators.
 // NT loads carry the nontemporal hint (streamed weights are not re-read).
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
 template <class T, bool NT>
 __device__ inline T load_hint(const T* p)
 {
@@ -216,18 +215,8 @@ struct Chunk<1, NT> {  // any N, any alignment
     __device__ void add(int32_t* acc) const { acc[0] += (int32_t)v; }
 };
 
-// The same loads through a buffer resource (base and size in scalar
-// registers, a 32-bit byte offset per lane): no 64-bit address arithmetic,
-// and an offset at or past the resource's size reads as zero without a
-// memory access.  NT sets the nontemporal cache policy.
-constexpr uint32_t kOutOfRange = 0x80000000u;  // offset that is always past the resource
-constexpr int64_t kBufMaxBytes = 0x7fffff00;   // largest weight matrix the buffer path addresses
-constexpr int kBufferFlags = 0x00020000;       // buffer resource word 3: 32-bit data format (gfx9)
-
-__device__ inline __amdgpu_buffer_rsrc_t weight_resource(const int8_t* base, int64_t bytes)
-{
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(base), 0, (int)bytes, kBufferFlags);
-}
+// The same loads through a buffer resource (buffer.hpp): offsets past the
+// resource read as zero.  NT sets the nontemporal cache policy.
 
 template <int V, bool NT>
 struct BufChunk;
@@ -414,8 +403,6 @@ __device__ inline void store_result(float* out_row, int32_t* acc_row, const floa
 // stores: a tile then costs two store instructions instead of eight, and
 // narrow stores stall the in-order vector memory pipeline of the CU (every
 // weight load queued behind a store waits with it).
-typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 template <class S, bool ACC>
 __device__ inline void finish_tile(const int32_t* red, int64_t n_tile0, int N, const float* __restrict__ scale,

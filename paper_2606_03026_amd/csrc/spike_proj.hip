@@ -16,6 +16,7 @@
 #include <string>
 #include <vector>
 
+#include "errors.hpp"
 #include "gather.hpp"
 #include "mfma.hpp"
 
@@ -24,20 +25,8 @@ struct spike_stream;
 
 namespace {
 
-thread_local std::string g_last_error;
-
-int fail(int code, const char* fmt, ...)
-{
-    char buf[512];
-    va_list ap;
-    va_start(ap, fmt);
-    vsnprintf(buf, sizeof buf, fmt, ap);
-    va_end(ap);
-    g_last_error = buf;
-    return code;
-}
-
-int hip_fail(hipError_t e, const char* what) { return fail(SPIKE_EHIP, "%s: %s", what, hipGetErrorString(e)); }
+using spk::fail;
+using spk::hip_fail;
 
 int64_t words_per_row(int64_t K) { return (K + 63) / 64; }
 
@@ -505,7 +494,7 @@ extern "C" {
 int spike_proj_create_reserved(const int8_t* W, const float* scale, int32_t K, int32_t N, int32_t max_B,
                                int32_t flags, spike_proj_t* out_handle)
 {
-    g_last_error.clear();
+    spk::last_error.clear();
     if (!out_handle)
         return fail(SPIKE_EINVAL, "null out_handle");
     *out_handle = nullptr;
@@ -558,7 +547,7 @@ int spike_proj_create(const int8_t* W, const float* scale, int32_t K, int32_t N,
 
 int spike_proj_reserve(spike_proj_t h, int32_t max_B)
 {
-    g_last_error.clear();
+    spk::last_error.clear();
     if (!h)
         return fail(SPIKE_EINVAL, "null handle");
     if (max_B < 1 || max_B > 65535)
@@ -597,7 +586,7 @@ int spike_proj_forward_acc(spike_proj_t h, const uint64_t* mask, int32_t B, int3
 int spike_proj_forward_noalloc(const int8_t* W, const float* scale, int32_t K, int32_t N, const uint64_t* mask,
                                int32_t B, float* out, void* stream)
 {
-    g_last_error.clear();
+    spk::last_error.clear();
     if (K < 1 || K > SPIKE_MAX_K)
         return fail(SPIKE_EINVAL, "K = %d outside [1, %d]", K, SPIKE_MAX_K);
     if (N < 1 || N > SPIKE_MAX_N)
@@ -660,7 +649,7 @@ int spike_proj_destroy(spike_proj_t h)
 
 int spike_proj_tune(spike_proj_t h, int32_t key, int32_t value)
 {
-    g_last_error.clear();
+    spk::last_error.clear();
     if (!h)
         return fail(SPIKE_EINVAL, "null handle");
     switch (key) {
@@ -732,7 +721,7 @@ int spike_proj_tune(spike_proj_t h, int32_t key, int32_t value)
 int spike_compact(const uint64_t* mask, int32_t B, int32_t K, int32_t* active_idx, int32_t* active_count,
                   void* stream)
 {
-    g_last_error.clear();
+    spk::last_error.clear();
     if (B < 0 || K < 1 || K > SPIKE_MAX_K)
         return fail(SPIKE_EINVAL, "B = %d or K = %d out of range", B, K);
     if (B == 0)
@@ -748,7 +737,7 @@ int spike_compact(const uint64_t* mask, int32_t B, int32_t K, int32_t* active_id
 int spike_stack_forward(const spike_proj_t* projs, int32_t n_proj, const uint64_t* masks, int32_t B, float* out,
                         void* stream)
 {
-    g_last_error.clear();
+    spk::last_error.clear();
     if (!projs || n_proj < 1)
         return fail(SPIKE_EINVAL, "need at least one projection");
     if (B < 0)
@@ -776,7 +765,7 @@ int spike_stack_forward(const spike_proj_t* projs, int32_t n_proj, const uint64_
 int spike_stack_forward_fused(const spike_proj_t* projs, int32_t n_proj, const uint64_t* masks, int32_t B,
                               float* out, void* stream)
 {
-    g_last_error.clear();
+    spk::last_error.clear();
     if (!projs || n_proj < 1)
         return fail(SPIKE_EINVAL, "need at least one projection");
     if (n_proj > spk::kMfmaMaxItems)
@@ -853,7 +842,7 @@ int spike_stack_forward_fused(const spike_proj_t* projs, int32_t n_proj, const u
 int spike_stream_create(const spike_proj_t* projs, int32_t n_proj, int32_t n_sets, int32_t n_tokens,
                         spike_stream_t* out_stream)
 {
-    g_last_error.clear();
+    spk::last_error.clear();
     if (!out_stream)
         return fail(SPIKE_EINVAL, "null out_stream");
     *out_stream = nullptr;
@@ -948,7 +937,7 @@ int spike_stream_create(const spike_proj_t* projs, int32_t n_proj, int32_t n_set
 
 int spike_stream_tune(spike_stream_t s, int32_t key, int32_t value)
 {
-    g_last_error.clear();
+    spk::last_error.clear();
     if (!s)
         return fail(SPIKE_EINVAL, "null stream handle");
     switch (key) {
@@ -981,7 +970,7 @@ int spike_stream_tune(spike_stream_t s, int32_t key, int32_t value)
 
 int spike_stream_forward(spike_stream_t s, const uint64_t* masks, float* out, void* stream)
 {
-    g_last_error.clear();
+    spk::last_error.clear();
     if (!s)
         return fail(SPIKE_EINVAL, "null stream handle");
     if (!masks || !out)
@@ -1029,7 +1018,7 @@ int spike_mfma_plans(int32_t* codes, int32_t cap) { return spk::mfma_plan_codes(
 
 int spike_proj_plan_query(int32_t K, int32_t N, int32_t B, int32_t* path, int32_t* plan)
 {
-    g_last_error.clear();
+    spk::last_error.clear();
     if (!path || !plan)
         return fail(SPIKE_EINVAL, "null output pointer");
     if (K < 1 || K > SPIKE_MAX_K || N < 1 || N > SPIKE_MAX_N || B < 0)
@@ -1041,7 +1030,7 @@ int spike_proj_plan_query(int32_t K, int32_t N, int32_t B, int32_t* path, int32_
     return SPIKE_OK;
 }
 
-const char* spike_proj_last_error(void) { return g_last_error.c_str(); }
+const char* spike_proj_last_error(void) { return spk::last_error.c_str(); }
 
 int spike_proj_abi_version(void) { return SPIKE_PROJ_ABI_VERSION; }
 

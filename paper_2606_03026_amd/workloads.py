@@ -38,7 +38,16 @@ PROJ_SHAPES = {PROJ_TCAM: (RESIDUAL, RESIDUAL), PROJ_DOWN: (FFN_HIDDEN, RESIDUAL
 _P_W, _P_SCALE, _P_MASK, _P_RATE, _P_HOT, _P_ROWRATE = 0, 1, 2, 3, 4, 5
 
 # Workload ids (first seed word after 42).
-W_SINGLE, W_DOWN_SWEEP, W_STACK, W_PREFILL, W_BATCHED_STACK, W_TESTS = 1, 2, 3, 4, 5, 9
+W_SINGLE, W_DOWN_SWEEP, W_STACK, W_PREFILL, W_BATCHED_STACK, W_DENSE, W_TESTS = 1, 2, 3, 4, 5, 6, 9
+
+# Continuous-input projections of one block and the head (Sec. 2.1): row-major
+# INT8 weights [M, K] applied to FP32 activations.  (K, M) per kind.
+VOCAB = 57344            # output vocabulary slots of the deployed model (Sec. 2.1)
+DENSE_SHAPES = {
+    "qkvo": (RESIDUAL, RESIDUAL),      # attention query/key/value/output, 1536 -> 1536
+    "up": (RESIDUAL, FFN_HIDDEN),      # FFN up projection, 1536 -> 6144
+    "head": (RESIDUAL, VOCAB),         # vocabulary output projection, 1536 -> 57344
+}
 
 DOWN_SWEEP_RATES = (0.02, 0.05, 0.10, 0.20, 0.40)
 
@@ -211,6 +220,32 @@ def batched_stack_bits(layer: int, proj: int, B: int = 64, n_steps: int = 16,
     prob[:, hot] = hot_p
     u = rng_for(W_BATCHED_STACK, layer, proj, _P_MASK).random((n_steps, B, K))
     return u < prob[None]
+
+
+def dense_projection(kind: str, B: int = 1):
+    """Row-major INT8 weights Q [M, K] ~ rounded N(0, 30), scales on
+    [1e-3, 1e-2] and FP32 activations x [B, K] ~ N(0, 1) (the scale of a
+    layer-normalised residual stream) for one continuous-input projection."""
+    K, M = DENSE_SHAPES[kind]
+    proj = list(DENSE_SHAPES).index(kind)
+    Q = gaussian_weights(rng_for(W_DENSE, 0, proj, _P_W), M, K)
+    s = uniform_scales(rng_for(W_DENSE, 0, proj, _P_SCALE), M)
+    x = rng_for(W_DENSE, 0, proj, _P_MASK).standard_normal((B, K)).astype(np.float32)
+    return dict(Q=Q, scale=s, x=x, K=K, M=M, B=B)
+
+
+def dense_problem(M: int, K: int, B: int, seed: int = 0, integer_x: bool = False):
+    """Small seeded dense problem of any shape.  integer_x draws x from the
+    integers in [-8, 8], so that every partial sum of |Q x| stays an exact
+    FP32 integer for K up to 16,512."""
+    rng = np.random.default_rng([SEED, W_TESTS, 1, M, K, B, seed])
+    Q = rng.integers(-127, 127, size=(M, K), dtype=np.int8, endpoint=True)
+    s = uniform_scales(rng, M)
+    if integer_x:
+        x = rng.integers(-8, 8, size=(B, K), endpoint=True).astype(np.float32)
+    else:
+        x = rng.standard_normal((B, K)).astype(np.float32)
+    return dict(Q=Q, scale=s, x=x, K=K, M=M, B=B)
 
 
 def small_problem(K: int, N: int, B: int, p: float, seed: int = 0, w_lo: int = -127, w_hi: int = 127):

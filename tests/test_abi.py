@@ -21,13 +21,13 @@ def declared_functions():
     names = set()
     for hdr in glob.glob(os.path.join(ROOT, "include", "*.h")):
         text = re.sub(r"/\*.*?\*/", "", open(hdr).read(), flags=re.S)
-        names |= set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(spike_\w+)\s*\(", text, flags=re.M))
+        names |= set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*((?:spike|dense)_\w+)\s*\(", text, flags=re.M))
     return sorted(names)
 
 
 def test_header_declares_the_entry_points():
     names = declared_functions()
-    for required in ("spike_proj_create", "spike_proj_forward", "spike_proj_destroy"):
+    for required in ("spike_proj_create", "spike_proj_forward", "spike_proj_destroy", "dense_proj_forward"):
         assert required in names
 
 
@@ -109,6 +109,64 @@ def test_automatic_matrix_core_plans_are_instantiated(sp):
     path, plan = sp.spike_proj_plan_query(6144, 1536, 512)
     assert path == sp.SPIKE_PATH_MFMA and plan["rt"] == 4
     assert sp.spike_proj_plan_query(1536, 1000, 1)[0] == sp.SPIKE_PATH_GATHER
+
+
+def test_dense_argument_validation_before_any_hip_call(sp):
+    lib = sp.raw_library()
+    d = 0x1000  # never dereferenced: validation fails first
+    assert lib.dense_proj_forward(d, d, 0, 4, d, 1, d, None) == sp.SPIKE_EINVAL
+    assert "K = 0" in sp.spike_proj_last_error()
+    assert lib.dense_proj_forward(d, d, sp.DENSE_MAX_K + 1, 4, d, 1, d, None) == sp.SPIKE_EINVAL
+    assert lib.dense_proj_forward(d, d, 64, 0, d, 1, d, None) == sp.SPIKE_EINVAL
+    assert lib.dense_proj_forward(d, d, 16000, 1 << 18, d, 1, d, None) == sp.SPIKE_EUNSUPPORTED
+    assert "exceeds" in sp.spike_proj_last_error()
+    assert lib.dense_proj_forward(d, d, 64, 4, d, -1, d, None) == sp.SPIKE_EINVAL
+    assert lib.dense_proj_forward(d, d, 64, 4, d, sp.DENSE_MAX_B + 1, d, None) == sp.SPIKE_EINVAL
+    assert lib.dense_proj_forward(None, d, 64, 4, d, 1, d, None) == sp.SPIKE_EINVAL
+    assert "null" in sp.spike_proj_last_error()
+    assert lib.dense_proj_forward(d, d, 64, 4, d + 2, 1, d, None) == sp.SPIKE_EINVAL
+    assert lib.dense_proj_forward(None, None, 64, 4, None, 0, None, None) == sp.SPIKE_OK  # B = 0: nothing to do
+    assert sp.spike_proj_last_error() == ""
+
+
+def test_dense_plans(sp):
+    """Kernel and load width follow K and Q's alignment only; a launch takes up
+    to 4 (register kernel) or 8 (staged kernel) batch rows; the vocabulary head
+    spreads over at least two workgroups per CU."""
+    reg, staged = sp.DENSE_KERNEL_REGISTER, sp.DENSE_KERNEL_STAGED
+    head = sp.dense_proj_plan(1536, 57344, 1)
+    assert (head["kernel"], head["vec"]) == (reg, 16)
+    assert head["workgroups"] >= 512
+    for B in (1, 2, 3, 8, 13):
+        assert sp.dense_proj_plan(1536, 57344, B)["kernel"] == reg
+    assert sp.dense_proj_plan(1536, 57344, 1, q_align=4)["kernel"] == staged
+    assert sp.dense_proj_plan(1536, 57344, 1, q_align=4)["vec"] == 4
+    assert sp.dense_proj_plan(1536, 57344, 1, q_align=8)["vec"] == 4
+    assert sp.dense_proj_plan(1540, 100, 1)["vec"] == 4
+    assert sp.dense_proj_plan(1537, 100, 1)["vec"] == 1
+    assert sp.dense_proj_plan(1536, 100, 1, q_align=2)["vec"] == 1
+    assert sp.dense_proj_plan(4096, 100, 1)["kernel"] == reg
+    assert sp.dense_proj_plan(4112, 100, 1)["kernel"] == staged
+    assert [sp.dense_proj_plan(512, 100, B)["rows_per_launch"] for B in (1, 2, 3, 5, 8)] == [1, 2, 4, 4, 4]
+    assert [sp.dense_proj_plan(1536, 100, B)["rows_per_launch"] for B in (1, 2, 3)] == [1, 2, 2]
+    assert [sp.dense_proj_plan(2048, 100, B)["rows_per_launch"] for B in (1, 2, 3)] == [1, 1, 1]
+    assert [sp.dense_proj_plan(1540, 100, B)["rows_per_launch"] for B in (1, 2, 3, 5, 8, 13)] == [1, 2, 4, 8, 8, 8]
+    assert sp.dense_proj_plan(sp.DENSE_MAX_K, 3, 8)["rows_per_launch"] == 1  # LDS holds one row of the largest K
+    with pytest.raises(sp.SpikeError):
+        sp.dense_proj_plan(64, 4, 1, q_align=3)
+    try:
+        sp.dense_proj_tune(sp.DENSE_TUNE_KERNEL, staged)
+        assert sp.dense_proj_plan(1536, 57344, 1)["kernel"] == staged
+        sp.dense_proj_tune(sp.DENSE_TUNE_WG_PER_CU, 2)
+        sp.dense_proj_tune(sp.DENSE_TUNE_KERNEL, 0)
+        assert sp.dense_proj_plan(1536, 57344, 1)["workgroups"] == 512
+        with pytest.raises(sp.SpikeError):
+            sp.dense_proj_tune(sp.DENSE_TUNE_KERNEL, 7)
+        with pytest.raises(sp.SpikeError):
+            sp.dense_proj_tune(99, 0)
+    finally:
+        sp.dense_proj_tune(sp.DENSE_TUNE_KERNEL, 0)
+        sp.dense_proj_tune(sp.DENSE_TUNE_WG_PER_CU, 0)
 
 
 def test_create_rejects_unknown_flags(sp):
