@@ -46,7 +46,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_stream_decode_stack_traffic.jso
 # The timed kernel: the stream kernel of gather.hpp at this launch shape
 # (16 bytes per lane, 32-lane groups, 4 columns in flight, 256 threads,
 # nontemporal loads).  The traffic record is keyed on both.
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_03026_amd", "csrc", "gather.hpp")]
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_03026_amd", "csrc", f) for f in ("gather.hpp", "buffer.hpp")]
 HEADLINE_SHAPE = (16, 32, 4, 256, True)
 
 
@@ -263,6 +263,96 @@ def cold_copies(bytes_per_mask: float, n_masks: int) -> int:
     return int(min(n_masks, max(32, np.ceil(2 * MALL_BYTES / bytes_per_mask))))
 
 
+def bench_dense(sp, torch, wl, timer, batches=(1, 2)):
+    """The continuous-input projections (row-major INT8 weights, FP32
+    activations): attention 1536->1536, FFN up 1536->6144 and the vocabulary
+    head 1536->57344.  Per call: `calls` launches in one graph, each on the
+    next of `copies` weight copies, with copies * weight bytes >= 2x the
+    Infinity Cache, so every call streams its weights from HBM.  Bytes per
+    call: weights + scales + activations in + outputs."""
+    res = {}
+    for kind in wl.DENSE_SHAPES:
+        d = wl.dense_projection(kind, B=max(batches))
+        M, K = d["Q"].shape
+        copies = int(max(1, np.ceil(2 * MALL_BYTES / (M * K))))
+        Qs = [torch.from_numpy(d["Q"]).cuda() for _ in range(copies)]
+        s = torch.from_numpy(d["scale"]).cuda()
+        x = torch.from_numpy(d["x"]).cuda()
+        y = torch.empty((max(batches), M), dtype=torch.float32, device="cuda")
+        calls = max(copies, 64)
+        for B in batches:
+            g = graph_of(torch, lambda: [sp.dense_proj_forward(Qs[i % copies], s, x, B, y) for i in range(calls)])
+            sec = timer(g.replay, 3, 1) / calls
+            del g
+            byts = M * K + 4 * M + 4 * B * (K + M)
+            plan = sp.dense_proj_plan(K, M, B)
+            r = {"K": K, "M": M, "B": B, "bytes_per_call": byts, "call_us": round(sec * 1e6, 2),
+                 "gbs": round(byts / sec / 1e9, 1), "hbm_frac": round(byts / sec / 1e9 / HBM_PEAK_GBS, 4),
+                 "weight_copies": copies,
+                 "kernel": "register" if plan["kernel"] == sp.DENSE_KERNEL_REGISTER else "staged",
+                 "launches_per_call": -(-B // plan["rows_per_launch"])}
+            log(f"dense {kind} {K}->{M} B={B}: {r['call_us']} us per call, {r['gbs']} GB/s "
+                f"({100 * r['hbm_frac']:.1f}% of HBM), {r['kernel']} kernel")
+            res[f"{kind}_{K}x{M}_b{B}"] = r
+        del Qs
+        torch.cuda.empty_cache()
+    return res
+
+
+def write_traffic_record(fetch_csv: str, write_csv: str, steps: int, warmup: int, tokens: int) -> int:
+    """Assemble the HBM-traffic record of the headline stream kernel from two
+    rocprofv3 --pmc runs of `bench.py --only-stream --copy-probe` (one with
+    FETCH_SIZE, one with WRITE_SIZE; KiB per dispatch).  Each counter is
+    scaled by what it reads for the 1 GiB copy of --copy-probe.  The first
+    warmup + steps stream dispatches are the cold (rotated-copies) ones."""
+    import csv
+    from paper_2606_03026_amd import workloads as wl
+
+    def rows(path, counter):
+        out = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        out.sort(key=lambda r: int(r["Dispatch_Id"]))
+        copy = max((r for r in out if r["Kernel_Name"].startswith("__amd_rocclr_copyBuffer")),
+                   key=lambda r: float(r["Counter_Value"]))
+        stream = [float(r["Counter_Value"]) for r in out if "spk::k_stream<" in r["Kernel_Name"]]
+        return float(copy["Counter_Value"]), stream
+
+    gib_kib = float(1 << 20)
+    f_copy, fetch = rows(fetch_csv, "FETCH_SIZE")
+    w_copy, write = rows(write_csv, "WRITE_SIZE")
+    n_cold = warmup + steps
+    f_scale, w_scale = gib_kib / f_copy, gib_kib / w_copy
+    fetch_bytes = float(np.mean(fetch[:n_cold])) * 1024 * f_scale
+    write_bytes = float(np.mean(write[:n_cold])) * 1024 * w_scale
+    order = wl.stack_order()
+    Ks = [wl.PROJ_SHAPES[j][0] for (_, j) in order]
+    algo = int(active_counts(wl.stack_token_masks(tokens), Ks).sum()) * wl.RESIDUAL
+    cmd = ("rocprofv3 --pmc {c} -d gpurun_out/pmc_{c} -o pmc --output-format csv -- python3 -u bench.py "
+           f"--only-stream --copy-probe --steps {steps} --warmup {warmup} --no-cpu")
+    rec = {
+        "kernel": f"k_stream<Shape{HEADLINE_SHAPE}, buffer loads> on the {tokens}-token 22-block decode stream",
+        "kernel_source_hash": kernel_source_hash(),
+        "command_fetch": cmd.format(c="FETCH_SIZE"),
+        "command_write": cmd.format(c="WRITE_SIZE"),
+        "command_record": (f"python3 bench.py --traffic-record gpurun_out/pmc_FETCH_SIZE/pmc_counter_collection.csv "
+                           f"gpurun_out/pmc_WRITE_SIZE/pmc_counter_collection.csv --steps {steps} --warmup {warmup}"),
+        "calibration": {"kernel": "__amd_rocclr_copyBuffer, 1 GiB read + 1 GiB written (bench.py --copy-probe)",
+                        "fetch_kib": f_copy, "write_kib": w_copy,
+                        "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)},
+        "raw_kib_per_launch": {"fetch_cold": [round(v, 1) for v in fetch[:n_cold]],
+                               "fetch_warm": [round(v, 1) for v in fetch[n_cold:]],
+                               "write": [round(v, 1) for v in write]},
+        "fetch_bytes_per_launch": round(fetch_bytes),
+        "write_bytes_per_launch": round(write_bytes),
+        "hbm_bytes_per_launch": round(fetch_bytes + write_bytes),
+        "algorithmic_active_bytes_per_launch": algo,
+        "fetch_over_algorithmic": round(fetch_bytes / algo, 4),
+    }
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps({k: rec[k] for k in ("hbm_bytes_per_launch", "fetch_over_algorithmic", "kernel_source_hash")}))
+    return 0
+
+
 def bench_prefill(sp, torch, wl, timer):
     d = wl.prefill_projection()
     B, K, N = d["masks"].shape[0], d["K"], d["N"]
@@ -377,7 +467,14 @@ def main(argv=None) -> int:
                     help="time only the matrix-core workloads, prefill and batched stack (for profiling)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a 1 GiB device copy first (reference for the PMC byte counters)")
+    ap.add_argument("--only-dense", action="store_true",
+                    help="time only the continuous-input projections (for profiling)")
+    ap.add_argument("--traffic-record", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the stream kernel's HBM-traffic record from two rocprofv3 --pmc CSVs (no GPU)")
     args = ap.parse_args(argv)
+
+    if args.traffic_record:
+        return write_traffic_record(*args.traffic_record, args.steps, args.warmup, args.tokens)
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
@@ -407,6 +504,9 @@ def main(argv=None) -> int:
                "batched_stack_b64": bench_batched_stack(sp, torch, wl, timer)}
         print(json.dumps({"workloads": res}), flush=True)
         return 0
+    if args.only_dense:
+        print(json.dumps({"workloads": {"dense": bench_dense(sp, torch, wl, timer)}}), flush=True)
+        return 0
     if args.only_stream:
         args.no_latency = True
     main_res = bench_decode_stack(sp, torch, wl, timer, args)
@@ -427,6 +527,7 @@ def main(argv=None) -> int:
         del downs
         extra["prefill_512x6144x1536"] = bench_prefill(sp, torch, wl, timer)
         extra["batched_stack_b64"] = bench_batched_stack(sp, torch, wl, timer)
+        extra["dense"] = bench_dense(sp, torch, wl, timer)
 
     cpu = None
     if not args.no_cpu:
