@@ -4,3 +4,4 @@ Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
 import this package.  The GPU library never uses it.
 """
 from .spike_oracle import build, load, active_indices, spike_acc, spike_forward, dense_forward  # noqa: F401
+from .quant_oracle import quantize_int8, export_column_major  # noqa: F401

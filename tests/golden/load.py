@@ -71,3 +71,32 @@ def load_dense_example(name: str = "dense_hand_example.txt"):
     Q = np.array(Q, dtype=np.int8)
     assert Q.shape == (M, K)
     return dict(M=M, K=K, Q=Q, scale=scale, x=np.array(x, dtype=np.float32), y=np.array(y, dtype=np.float64))
+
+
+def load_quant_example(name: str = "quant_hand_example.txt"):
+    """The hand-worked quantizer example: W [M, K] f32, Q [M, K] int8 and the
+    scales, with None where the fixture says "floor" (the 1e-8 floor's scale)."""
+    W, Q, scale = [], [], None
+    M = K = None
+    with open(os.path.join(HERE, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            key, *vals = line.split()
+            if key == "M":
+                M = int(vals[0])
+            elif key == "K":
+                K = int(vals[0])
+            elif key == "W":
+                W.append([float(v) for v in vals])
+            elif key == "Q":
+                Q.append([int(v) for v in vals])
+            elif key == "scale":
+                scale = [None if v == "floor" else float(v) for v in vals]
+            else:
+                raise ValueError(f"unknown key {key}")
+    W = np.array(W, dtype=np.float32)
+    Q = np.array(Q, dtype=np.int8)
+    assert W.shape == Q.shape == (M, K) and len(scale) == M
+    return dict(M=M, K=K, W=W, Q=Q, scale=scale)
