@@ -299,6 +299,36 @@ def bench_dense(sp, torch, wl, timer, batches=(1, 2)):
     return res
 
 
+def bench_quantize(sp, torch, wl, timer):
+    """The exporter's symmetric per-channel INT8 quantization on the model's
+    largest matrices: FFN down [1536][6144] into the column-major spike
+    layout and the vocabulary head [57344][1536] into the row-major dense
+    layout.  Algorithmic bytes: W read once (4 B/element), Q written once
+    (1 B/element), scales written; the kernels read W twice (scale pass,
+    then quantize pass), so 9 B/element move."""
+    res = {}
+    for name, (M, K), layout in (("down_col", (1536, 6144), sp.SPIKE_LAYOUT_COL_MAJOR),
+                                 ("head_row", (wl.VOCAB, 1536), sp.SPIKE_LAYOUT_ROW_MAJOR)):
+        rng = np.random.default_rng([42, 14, M, K])
+        W = torch.from_numpy(rng.normal(0.0, 0.02, size=(M, K)).astype(np.float32)).cuda()
+        Q = torch.empty(M * K, dtype=torch.int8, device="cuda")
+        s = torch.empty(M, dtype=torch.float32, device="cuda")
+        g = graph_of(torch, lambda: [sp.spike_quantize_int8(W, layout, Q, s) for _ in range(10)])
+        sec = timer(g.replay, 3, 1) / 10
+        del g
+        algo = 5 * M * K + 4 * M
+        moved = 9 * M * K + 4 * M
+        r = {"M": M, "K": K, "layout": "col" if layout == sp.SPIKE_LAYOUT_COL_MAJOR else "row",
+             "call_us": round(sec * 1e6, 2), "algorithmic_gbs": round(algo / sec / 1e9, 1),
+             "moved_gbs": round(moved / sec / 1e9, 1), "hbm_frac_moved": round(moved / sec / 1e9 / HBM_PEAK_GBS, 4)}
+        log(f"quantize {name} [{M}][{K}]: {r['call_us']} us, {r['algorithmic_gbs']} GB/s algorithmic, "
+            f"{r['moved_gbs']} GB/s moved ({100 * r['hbm_frac_moved']:.1f}% of HBM)")
+        res[name] = r
+        del W, Q, s
+        torch.cuda.empty_cache()
+    return res
+
+
 def write_traffic_record(fetch_csv: str, write_csv: str, steps: int, warmup: int, tokens: int) -> int:
     """Assemble the HBM-traffic record of the headline stream kernel from two
     rocprofv3 --pmc runs of `bench.py --only-stream --copy-probe` (one with
@@ -468,7 +498,7 @@ def main(argv=None) -> int:
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a 1 GiB device copy first (reference for the PMC byte counters)")
     ap.add_argument("--only-dense", action="store_true",
-                    help="time only the continuous-input projections (for profiling)")
+                    help="time only the continuous-input projections and the quantizer (for profiling)")
     ap.add_argument("--traffic-record", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the stream kernel's HBM-traffic record from two rocprofv3 --pmc CSVs (no GPU)")
     args = ap.parse_args(argv)
@@ -505,7 +535,8 @@ def main(argv=None) -> int:
         print(json.dumps({"workloads": res}), flush=True)
         return 0
     if args.only_dense:
-        print(json.dumps({"workloads": {"dense": bench_dense(sp, torch, wl, timer)}}), flush=True)
+        print(json.dumps({"workloads": {"dense": bench_dense(sp, torch, wl, timer),
+                                        "quantize": bench_quantize(sp, torch, wl, timer)}}), flush=True)
         return 0
     if args.only_stream:
         args.no_latency = True
@@ -528,6 +559,7 @@ def main(argv=None) -> int:
         extra["prefill_512x6144x1536"] = bench_prefill(sp, torch, wl, timer)
         extra["batched_stack_b64"] = bench_batched_stack(sp, torch, wl, timer)
         extra["dense"] = bench_dense(sp, torch, wl, timer)
+        extra["quantize"] = bench_quantize(sp, torch, wl, timer)
 
     cpu = None
     if not args.no_cpu:

@@ -1,5 +1,5 @@
-"""ctypes binding of libspike_proj.so (C ABI in include/spike_proj.h and
-include/dense_proj.h).
+"""ctypes binding of libspike_proj.so (C ABI in include/spike_proj.h,
+include/dense_proj.h and include/quantize.h).
 
 Argument marshalling only: every step of the projection runs in the HIP
 kernels of the library.  Tensors are torch device tensors; their data
@@ -25,6 +25,7 @@ SPIKE_DEFAULT_MAX_B = 512
 DENSE_MAX_K, DENSE_MAX_B = 16128, 65535
 DENSE_KERNEL_STAGED, DENSE_KERNEL_REGISTER = 1, 2
 DENSE_TUNE_KERNEL, DENSE_TUNE_WG_PER_CU = 1, 2
+SPIKE_LAYOUT_ROW_MAJOR, SPIKE_LAYOUT_COL_MAJOR = 0, 1
 
 
 def SPIKE_SHAPE(V: int, LG: int, U: int, BLOCK: int, NT: bool = False) -> int:
@@ -38,6 +39,7 @@ EXPORTED = (
     "spike_proj_last_error", "spike_proj_shapes", "spike_mfma_plans", "spike_proj_plan_query",
     "spike_proj_abi_version", "spike_proj_forward_noalloc", "spike_proj_create_reserved",
     "spike_stack_forward_fused", "dense_proj_forward", "dense_proj_plan", "dense_proj_tune",
+    "spike_quantize_int8", "spike_check_scale_shape",
 )
 
 if not os.path.exists(LIB):
@@ -68,6 +70,8 @@ _sig = {
     "dense_proj_forward": [_p, _p, _i32, _i32, _p, _i32, _p, _p],
     "dense_proj_plan": [_i32, _i32, _i32, _i32, _p, _p, _p, _p],
     "dense_proj_tune": [_i32, _i32],
+    "spike_quantize_int8": [_p, _i32, _i32, _i32, _p, _p, _p],
+    "spike_check_scale_shape": [_i32, _i32, _i32, _i32, _i32],
 }
 for _name, _args in _sig.items():
     getattr(_lib, _name).argtypes = _args
@@ -336,6 +340,23 @@ def dense_proj_plan(K: int, M: int, B: int, q_align: int = 16) -> dict:
 
 def dense_proj_tune(key: int, value: int) -> None:
     _check(_lib.dense_proj_tune(int(key), int(value)), "dense_proj_tune")
+
+
+def spike_quantize_int8(W: torch.Tensor, layout: int, Q: torch.Tensor, scale: torch.Tensor, stream=None) -> None:
+    """Symmetric per-channel INT8 quantization of W [M][K] (quantize.h): Q
+    int8 row-major [M][K] or column-major [K][M], scale float32 [M]."""
+    if W.dtype != torch.float32 or W.dim() != 2:
+        raise TypeError("W must be a 2-D float32 tensor [M][K]")
+    M, K = W.shape
+    if Q.dtype != torch.int8 or scale.dtype != torch.float32:
+        raise TypeError("Q must be int8 and scale float32")
+    _check(_lib.spike_quantize_int8(_dev_ptr(W, "W"), int(M), int(K), int(layout), _dev_ptr(Q, "Q", M * K),
+                                    _dev_ptr(scale, "scale", M * 4), _stream(stream)), "spike_quantize_int8")
+
+
+def spike_check_scale_shape(M: int, K: int, group: int, scale_rows: int, scale_cols: int) -> None:
+    _check(_lib.spike_check_scale_shape(int(M), int(K), int(group), int(scale_rows), int(scale_cols)),
+           "spike_check_scale_shape")
 
 
 def spike_proj_abi_version() -> int:

@@ -176,3 +176,33 @@ def test_create_rejects_unknown_flags(sp):
     assert lib.spike_proj_create_reserved(dummy, dummy, 4, 4, 1, 2, ctypes.byref(out)) == sp.SPIKE_EINVAL
     assert "flags" in sp.spike_proj_last_error()
     assert lib.spike_proj_create_reserved(dummy, dummy, 4, 4, 0, 0, ctypes.byref(out)) == sp.SPIKE_EINVAL
+
+
+def test_quantizer_argument_validation_before_any_hip_call(sp):
+    lib = sp.raw_library()
+    d = 0x1000  # never dereferenced: validation fails first
+    assert lib.spike_quantize_int8(d, 0, 4, 0, d, d, None) == sp.SPIKE_EINVAL
+    assert lib.spike_quantize_int8(d, 4, 0, 0, d, d, None) == sp.SPIKE_EINVAL
+    assert lib.spike_quantize_int8(d, 1 << 16, 1 << 16, 0, d, d, None) == sp.SPIKE_EINVAL
+    assert "2^31" in sp.spike_proj_last_error()
+    assert lib.spike_quantize_int8(d, 4, 4, 2, d, d, None) == sp.SPIKE_EINVAL
+    assert "layout" in sp.spike_proj_last_error()
+    assert lib.spike_quantize_int8(None, 4, 4, 0, d, d, None) == sp.SPIKE_EINVAL
+    assert lib.spike_quantize_int8(d + 2, 4, 4, 0, d, d, None) == sp.SPIKE_EINVAL
+
+
+def test_scale_shape_check_names_the_transposed_export(sp):
+    """The paper's withdrawn export: an FFN down weight [1536][6144] with
+    group 32 needs scales [1536][192]; scales taken after transposing have
+    shape [6144][48] -- the same element count -- and must be refused."""
+    sp.spike_check_scale_shape(1536, 6144, 32, 1536, 192)
+    sp.spike_check_scale_shape(1536, 6144, 6144, 1536, 1)  # per-channel
+    with pytest.raises(sp.SpikeError, match="transposed"):
+        sp.spike_check_scale_shape(1536, 6144, 32, 6144, 48)
+    with pytest.raises(sp.SpikeError, match="transposed"):
+        sp.spike_check_scale_shape(1536, 6144, 6144, 6144, 1)
+    with pytest.raises(sp.SpikeError, match="does not match"):
+        sp.spike_check_scale_shape(1536, 6144, 32, 1536, 193)
+    with pytest.raises(sp.SpikeError):
+        sp.spike_check_scale_shape(1536, 6144, 0, 1536, 192)
+    sp.spike_check_scale_shape(1536, 1536, 32, 1536, 48)  # square: the shapes coincide
