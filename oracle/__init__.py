@@ -5,3 +5,4 @@ import this package.  The GPU library never uses it.
 """
 from .spike_oracle import build, load, active_indices, spike_acc, spike_forward, dense_forward  # noqa: F401
 from .quant_oracle import quantize_int8, export_column_major  # noqa: F401
+from . import head_oracle  # noqa: F401

@@ -100,3 +100,33 @@ def load_quant_example(name: str = "quant_hand_example.txt"):
     Q = np.array(Q, dtype=np.int8)
     assert W.shape == Q.shape == (M, K) and len(scale) == M
     return dict(M=M, K=K, W=W, Q=Q, scale=scale)
+
+
+def load_head_example(name: str = "head_hand_example.txt"):
+    """The hand-worked head-verification example: x, xq, Q [V, K], scale,
+    approximate logits, candidate order, gap, recomputed logits (per row) and
+    (k, threshold, verified, token) cases."""
+    d = {"Q": [], "case": []}
+    with open(os.path.join(HERE, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            key, *vals = line.split()
+            if key in ("V", "K"):
+                d[key] = int(vals[0])
+            elif key == "Q":
+                d["Q"].append([int(v) for v in vals])
+            elif key == "case":
+                d["case"].append((int(vals[0]), float(vals[1]), bool(int(vals[2])), int(vals[3])))
+            elif key in ("x", "scale", "logits", "gap", "recomputed"):
+                d[key] = np.array([float(v) for v in vals], dtype=np.float64)
+            elif key in ("xq", "order"):
+                d[key] = np.array([int(v) for v in vals], dtype=np.int64)
+            else:
+                raise ValueError(f"unknown key {key}")
+    d["Q"] = np.array(d["Q"], dtype=np.int8)
+    d["x"] = d["x"].astype(np.float32)
+    d["scale"] = d["scale"].astype(np.float32)
+    assert d["Q"].shape == (d["V"], d["K"])
+    return d
