@@ -329,6 +329,44 @@ def bench_quantize(sp, torch, wl, timer):
     return res
 
 
+def bench_head_verify(sp, torch, wl, timer):
+    """The vocabulary head 1536 -> 57,344 with candidate verification (paper
+    Sec. 5): INT8-activation head over all rows + top-K selection, gate and
+    FP32 recompute of K rows, per token, against the FP32-activation dense
+    head over all rows (the paper's baseline configuration).  Cold weights:
+    calls rotate over copies whose bytes exceed 2x the Infinity Cache."""
+    d = wl.dense_projection("head", B=1)
+    V, K = d["Q"].shape
+    copies = int(max(1, np.ceil(2 * MALL_BYTES / (V * K))))
+    Qs = [torch.from_numpy(d["Q"]).cuda() for _ in range(copies)]
+    s = torch.from_numpy(d["scale"]).cuda()
+    x = torch.from_numpy(d["x"][0]).cuda()
+    logits = torch.empty(V, dtype=torch.float32, device="cuda")
+    cand = torch.empty(64, dtype=torch.int32, device="cuda")
+    cl = torch.empty(64, dtype=torch.float32, device="cuda")
+    res = torch.empty(2, dtype=torch.int32, device="cuda")
+    calls = max(copies, 64)
+    out = {"V": V, "K": K, "weight_copies": copies}
+    for k, thr, label in ((64, float("inf"), "k64_always_verify"), (64, 0.0, "k64_never_verify"),
+                          (16, 0.5, "k16_gate_0.5")):
+        g = graph_of(torch, lambda: [sp.head_verify_forward(Qs[i % copies], s, x, k, thr, logits, cand, cl, res)
+                                     for i in range(calls)])
+        sec = timer(g.replay, 3, 1) / calls
+        del g
+        out[label] = {"call_us": round(sec * 1e6, 2),
+                      "weight_gbs": round(V * K / sec / 1e9, 1),
+                      "hbm_frac": round(V * K / sec / 1e9 / HBM_PEAK_GBS, 4)}
+        log(f"head verify {label}: {out[label]['call_us']} us per token ({out[label]['weight_gbs']} GB/s of weights)")
+    y = torch.empty((1, V), dtype=torch.float32, device="cuda")
+    xb = x.view(1, K)
+    g = graph_of(torch, lambda: [sp.dense_proj_forward(Qs[i % copies], s, xb, 1, y) for i in range(calls)])
+    out["fp32_activation_head_us"] = round(timer(g.replay, 3, 1) / calls * 1e6, 2)
+    del g, Qs
+    torch.cuda.empty_cache()
+    log(f"head with FP32 activations (dense kernel): {out['fp32_activation_head_us']} us per token")
+    return out
+
+
 def write_traffic_record(fetch_csv: str, write_csv: str, steps: int, warmup: int, tokens: int) -> int:
     """Assemble the HBM-traffic record of the headline stream kernel from two
     rocprofv3 --pmc runs of `bench.py --only-stream --copy-probe` (one with
@@ -498,7 +536,8 @@ def main(argv=None) -> int:
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a 1 GiB device copy first (reference for the PMC byte counters)")
     ap.add_argument("--only-dense", action="store_true",
-                    help="time only the continuous-input projections and the quantizer (for profiling)")
+                    help="time only the continuous-input projections, the quantizer and the head verification "
+                         "(for profiling)")
     ap.add_argument("--traffic-record", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the stream kernel's HBM-traffic record from two rocprofv3 --pmc CSVs (no GPU)")
     args = ap.parse_args(argv)
@@ -536,7 +575,8 @@ def main(argv=None) -> int:
         return 0
     if args.only_dense:
         print(json.dumps({"workloads": {"dense": bench_dense(sp, torch, wl, timer),
-                                        "quantize": bench_quantize(sp, torch, wl, timer)}}), flush=True)
+                                        "quantize": bench_quantize(sp, torch, wl, timer),
+                                        "head_verify": bench_head_verify(sp, torch, wl, timer)}}), flush=True)
         return 0
     if args.only_stream:
         args.no_latency = True
@@ -560,6 +600,7 @@ def main(argv=None) -> int:
         extra["batched_stack_b64"] = bench_batched_stack(sp, torch, wl, timer)
         extra["dense"] = bench_dense(sp, torch, wl, timer)
         extra["quantize"] = bench_quantize(sp, torch, wl, timer)
+        extra["head_verify"] = bench_head_verify(sp, torch, wl, timer)
 
     cpu = None
     if not args.no_cpu:

@@ -1,0 +1,71 @@
+/*
+ * head_verify.h -- C ABI of the output-head candidate-row verification.
+ *
+ * Operation (paper Sec. 5, "Output-Head Power Case Study", projection-only
+ * trace configuration), for the vocabulary projection Q [V][K] (row-major
+ * INT8, one FP32 scale per row) and one FP32 activation vector x [K]:
+ *
+ *  1. x is quantized to INT8 with one scale for the vector, by the Sec. 2.3
+ *     formulas: s_x = max(max_k |x_k|, 1e-8) / 127, xq = clip(round(x / s_x),
+ *     -127, 127), in binary32 with ties to even;
+ *  2. approximate logits: logits[m] = fl32(fl32(acc_m) * fl32(scale[m] * s_x))
+ *     with acc_m = sum_k Q[m][k] xq_k exact in INT32;
+ *  3. candidates: the top_k rows with the largest approximate logits, largest
+ *     first, equal logits in ascending row order;
+ *  4. gate: gap = fl32(l(1) - l(2)) over the two largest approximate logits of
+ *     all V rows (+inf when V = 1); verification runs when gap < threshold;
+ *  5. verification: each candidate's logit recomputed with the FP32
+ *     activations, scale[m] * sum_k float(Q[m][k]) x_k (FP32 FMAs in a fixed
+ *     order: per lane a chain of at most 16 ceil(K/1024) products, a 6-level
+ *     lane tree, one multiply; error bound as for dense_proj.h with
+ *     h = 16 ceil(K/1024) + 7); the token
+ *     is the candidate with the largest recomputed logit (ties: lower row).
+ *     Without verification the token is the top candidate.
+ *
+ * Steps 1-3 and the gate decision are exact (bit-identical to the
+ * definition); step 5 is FP32 arithmetic within the stated bound.
+ *
+ * Arguments (DEVICE pointers):
+ *   Q            int8  [V][K] row-major, 16-byte aligned, K % 16 == 0,
+ *                16 <= K <= 4096, 1 <= V, V * K < 2^31.
+ *   scale        float [V].
+ *   x            float [K], 4-byte aligned.
+ *   top_k        1 <= top_k <= min(64, V).
+ *   threshold    gate threshold (not NaN; 0 never verifies, +inf verifies
+ *                whenever V >= 2).
+ *   logits       float [V] out: the approximate logits of step 2.
+ *   cand         int32 [top_k] out: candidate rows, best first.
+ *   cand_logits  float [top_k] out: the recomputed logits when verification
+ *                ran, else the candidates' approximate logits.
+ *   result       int32 [2] out: {token, 1 if verification ran else 0}.
+ * Two kernels are enqueued on `stream` (a hipStream_t, NULL for the default
+ * stream); the gate is decided on the device, so the call never waits for
+ * the GPU and can be captured in a HIP graph.  Nothing is allocated.
+ *
+ * Errors: SPIKE_OK (0) or a negative code from spike_proj.h, with the
+ * message in spike_proj_last_error(); arguments are validated before any
+ * HIP call.
+ */
+#ifndef HEAD_VERIFY_H
+#define HEAD_VERIFY_H
+
+#include <stdint.h>
+
+#include "spike_proj.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HEAD_MAX_TOP_K 64
+#define HEAD_MAX_K 4096
+
+int head_verify_forward(const int8_t *Q, const float *scale, int32_t K, int32_t V, const float *x, int32_t top_k,
+                        float threshold, float *logits, int32_t *cand, float *cand_logits, int32_t *result,
+                        void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HEAD_VERIFY_H */

@@ -1,5 +1,5 @@
 """ctypes binding of libspike_proj.so (C ABI in include/spike_proj.h,
-include/dense_proj.h and include/quantize.h).
+include/dense_proj.h, include/quantize.h and include/head_verify.h).
 
 Argument marshalling only: every step of the projection runs in the HIP
 kernels of the library.  Tensors are torch device tensors; their data
@@ -39,7 +39,7 @@ EXPORTED = (
     "spike_proj_last_error", "spike_proj_shapes", "spike_mfma_plans", "spike_proj_plan_query",
     "spike_proj_abi_version", "spike_proj_forward_noalloc", "spike_proj_create_reserved",
     "spike_stack_forward_fused", "dense_proj_forward", "dense_proj_plan", "dense_proj_tune",
-    "spike_quantize_int8", "spike_check_scale_shape",
+    "spike_quantize_int8", "spike_check_scale_shape", "head_verify_forward",
 )
 
 if not os.path.exists(LIB):
@@ -72,6 +72,7 @@ _sig = {
     "dense_proj_tune": [_i32, _i32],
     "spike_quantize_int8": [_p, _i32, _i32, _i32, _p, _p, _p],
     "spike_check_scale_shape": [_i32, _i32, _i32, _i32, _i32],
+    "head_verify_forward": [_p, _p, _i32, _i32, _p, _i32, ctypes.c_float, _p, _p, _p, _p, _p],
 }
 for _name, _args in _sig.items():
     getattr(_lib, _name).argtypes = _args
@@ -357,6 +358,25 @@ def spike_quantize_int8(W: torch.Tensor, layout: int, Q: torch.Tensor, scale: to
 def spike_check_scale_shape(M: int, K: int, group: int, scale_rows: int, scale_cols: int) -> None:
     _check(_lib.spike_check_scale_shape(int(M), int(K), int(group), int(scale_rows), int(scale_cols)),
            "spike_check_scale_shape")
+
+
+def head_verify_forward(Q: torch.Tensor, scale: torch.Tensor, x: torch.Tensor, top_k: int, threshold: float,
+                        logits: torch.Tensor, cand: torch.Tensor, cand_logits: torch.Tensor, result: torch.Tensor,
+                        stream=None) -> None:
+    """INT8-activation head, top-k candidates, gap gate, FP32 recompute (head_verify.h)."""
+    if Q.dtype != torch.int8 or Q.dim() != 2:
+        raise TypeError("Q must be a 2-D int8 tensor [V][K]")
+    V, K = Q.shape
+    for t, name, dt in ((scale, "scale", torch.float32), (x, "x", torch.float32), (logits, "logits", torch.float32),
+                        (cand, "cand", torch.int32), (cand_logits, "cand_logits", torch.float32),
+                        (result, "result", torch.int32)):
+        if t.dtype != dt:
+            raise TypeError(f"{name} must be {dt}")
+    k = int(top_k)
+    _check(_lib.head_verify_forward(_dev_ptr(Q, "Q"), _dev_ptr(scale, "scale", V * 4), int(K), int(V),
+                                    _dev_ptr(x, "x", K * 4), k, float(threshold), _dev_ptr(logits, "logits", V * 4),
+                                    _dev_ptr(cand, "cand", k * 4), _dev_ptr(cand_logits, "cand_logits", k * 4),
+                                    _dev_ptr(result, "result", 8), _stream(stream)), "head_verify_forward")
 
 
 def spike_proj_abi_version() -> int:

@@ -10,7 +10,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libspike_proj.so")
-SOURCES = [os.path.join(HERE, "csrc", f) for f in ("spike_proj.hip", "dense_proj.hip", "quantize.hip")]
+SOURCES = [os.path.join(HERE, "csrc", f) for f in (
+    "spike_proj.hip", "dense_proj.hip", "quantize.hip", "head_verify.hip")]
 DEPS = sorted(glob.glob(os.path.join(HERE, "csrc", "*"))) + sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

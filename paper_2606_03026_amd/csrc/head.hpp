@@ -1,0 +1,574 @@
+// Output-head candidate-row verification (gfx950).
+//
+// Paper Sec. 5 (projection-only configuration): the vocabulary projection
+// runs with INT8 activations over all V rows; when the gap between the two
+// largest of those approximate logits is below a threshold, the K
+// highest-scoring rows are recomputed with the FP32 activations and the
+// token is the best recomputed row; otherwise it is the approximate top row.
+//
+// k_head_approx: the activation vector is quantized with the Sec. 2.3
+// formulas (one scale for the vector, binary32, ties to even), each row's
+// integer dot product with the INT8 weights is exact (v_dot4 on four byte
+// pairs at a time, INT32), and the logit is fl32(fl32(acc) * fl32(s_m * s_x)).
+// The work split is the dense register kernel's: 32 lanes per row, each
+// lane's activation slice held in registers (here as packed INT8), a ring of
+// U rows of 16-byte weight loads in flight, rows q + Gq r per lane group,
+// results parked in lanes and stored 32 rows at a time.
+//
+// k_head_select: one workgroup of 1024 threads.  Finds the KK = max(K, 2)
+// largest logits on order-preserving 32-bit keys: a lower bound L on the
+// KK-th largest comes from the threads' maxima, the elements at or above L
+// (typically one to a few hundred) are pooled in LDS and each is placed by
+// its rank among them (equal logits by ascending row); when ties push the
+// pool past 1024 entries, a radix select over the whole array (digits of
+// 11, 11 and 10 bits, LDS histograms) picks the KK instead.  It then computes
+// the gap fl32(l(1) - l(2)) and, when it is below the threshold, recomputes
+// the K candidate rows with the FP32 activations (one wave per row: per
+// lane an FMA chain over its 16-byte chunks, a 6-level lane tree, one
+// multiply by s_m) and picks the largest (ties: the lower row).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "buffer.hpp"
+#include "dense.hpp"  // group32_sum's DPP helpers, kRegLanes, kRegGroups, kRegBlock
+
+namespace spk {
+
+constexpr int kHeadMaxK = 64;          // candidates
+constexpr int kSelectBlock = 1024;
+constexpr int kScanUnroll = 16;        // logits loaded per thread before any is used
+constexpr int kRegLogits = 56;         // heads up to 56 * 1024 = 57,344 rows are read into registers once
+constexpr int kHeadMaxChunks = 16;     // K <= 16 * 256 = 4096 in the recompute
+
+template <int CTRL>
+__device__ inline int add_dpp_int(int v)
+{
+    return v + __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+
+// Exact INT32 sum over the 32 lanes of a group (every lane gets it).
+__device__ inline int group32_sum_int(int v)
+{
+    v = add_dpp_int<0xB1>(v);
+    v = add_dpp_int<0x4E>(v);
+    v = add_dpp_int<0x141>(v);
+    v = add_dpp_int<0x140>(v);
+    return v + __builtin_amdgcn_ds_swizzle(v, 0x401F);
+}
+
+__device__ inline int8_t quant_act(float v, float s)
+{
+    return (int8_t)fminf(fmaxf(__builtin_rintf(__fdiv_rn(v, s)), -127.0f), 127.0f);
+}
+
+// s_x of the activation vector, computed by the whole workgroup.
+template <int BLOCK>
+__device__ inline float activation_scale(const float* __restrict__ x, int K, float* red)
+{
+    float amax = 0.0f;
+    for (int k = threadIdx.x; k < K; k += BLOCK)
+        amax = fmaxf(amax, fabsf(x[k]));
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1)
+        amax = fmaxf(amax, __shfl_xor(amax, d, 64));
+    if (threadIdx.x % 64 == 0)
+        red[threadIdx.x / 64] = amax;
+    __syncthreads();
+    float m = red[0];
+#pragma unroll
+    for (int w = 1; w < BLOCK / 64; ++w)
+        m = fmaxf(m, red[w]);
+    return __fdiv_rn(fmaxf(m, 1e-8f), 127.0f);
+}
+
+template <int NPL, int U>
+__global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restrict__ Q, const float* __restrict__ scale,
+                                                           int K, int V, const float* __restrict__ x,
+                                                           float* __restrict__ logits)
+{
+    __shared__ float red[kRegBlock / 64];
+    const int l = threadIdx.x % kRegLanes;
+    const int q = blockIdx.x * kRegGroups + threadIdx.x / kRegLanes;
+    const int Gq = gridDim.x * kRegGroups;
+    const int q_wave = q & ~1;
+    const int n_steps = __builtin_amdgcn_readfirstlane(q_wave < V ? (V - q_wave + Gq - 1) / Gq : 0);
+    const int n_chunks = K / 16;
+    const __amdgpu_buffer_rsrc_t qres = weight_resource(Q, (int64_t)V * K);
+    const __amdgpu_buffer_rsrc_t sres =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(scale), 0, V * 4, kBufferFlags);
+
+    uint32_t chunk_off[NPL];
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+        const int c = l + kRegLanes * j;
+        chunk_off[j] = c < n_chunks ? (uint32_t)(c * 16) : 0u;
+    }
+    auto row_base = [&](int r) -> uint32_t {
+        const int m = q + Gq * r;
+        return r < n_steps && m < V ? (uint32_t)m * (uint32_t)K : kOutOfRange;
+    };
+    // the first ring of weight loads goes out before the activation prologue
+    u32x4 slot[U][NPL];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const uint32_t base = row_base(u);
+#pragma unroll
+        for (int j = 0; j < NPL; ++j)
+            slot[u][j] = __builtin_amdgcn_raw_buffer_load_b128(qres, base + chunk_off[j], 0, 2);
+    }
+    const float sx = activation_scale<kRegBlock>(x, K, red);
+    // this lane's activations as packed INT8 (zeros past K)
+    uint32_t xq[NPL][4];
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+        const int c = l + kRegLanes * j;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            uint32_t packed = 0;
+            if (c < n_chunks) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    packed |= (uint32_t)(uint8_t)quant_act(x[c * 16 + 4 * i + t], sx) << (8 * t);
+            }
+            xq[j][i] = packed;
+        }
+    }
+    auto scale_of_step = [&](int rr) -> float {
+        const int m = q + Gq * rr;
+        const uint32_t off = rr < n_steps && m < V ? (uint32_t)m * 4u : kOutOfRange;
+        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(sres, off, 0, 0));
+    };
+    float sc = scale_of_step(l);
+    int parked = 0;
+    for (int r0 = 0; r0 < n_steps; r0 += U) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int r = r0 + u;
+            int acc = 0;
+#pragma unroll
+            for (int j = 0; j < NPL; ++j)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    acc = __builtin_amdgcn_sdot4((int)slot[u][j][i], (int)xq[j][i], acc, false);
+            {
+                const uint32_t base = row_base(r + U);
+#pragma unroll
+                for (int j = 0; j < NPL; ++j)
+                    slot[u][j] = __builtin_amdgcn_raw_buffer_load_b128(qres, base + chunk_off[j], 0, 2);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            const int tot = group32_sum_int(acc);
+            if (l == (r & 31))
+                parked = tot;
+            if (r < n_steps && ((r & 31) == 31 || r == n_steps - 1)) {
+                const int rr = (r & ~31) + l;
+                const int m = q + Gq * rr;
+                if (rr <= r && m < V) {
+                    const float c = sc * sx;
+                    logits[m] = (float)parked * c;
+                }
+                sc = scale_of_step((r & ~31) + 32 + l);
+            }
+        }
+    }
+}
+
+// Order-preserving key of a float: larger floats give larger keys.
+__device__ inline uint32_t order_key(float f)
+{
+    const uint32_t u = __builtin_bit_cast(uint32_t, f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ inline float key_value(uint32_t k)
+{
+    const uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+    return __builtin_bit_cast(float, u);
+}
+
+// Inclusive prefix sum over the 1024 threads of the workgroup (scan[] holds
+// one word per wave).
+__device__ inline int block_inclusive_scan(int v, int* scan)
+{
+    const int lane = threadIdx.x % 64, w = threadIdx.x / 64;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int t = __shfl_up(v, d, 64);
+        if (lane >= d)
+            v += t;
+    }
+    __syncthreads();
+    if (lane == 63)
+        scan[w] = v;
+    __syncthreads();
+    int before = 0;
+    for (int i = 0; i < w; ++i)
+        before += scan[i];
+    return v + before;
+}
+
+struct Entry {
+    uint32_t key;
+    int32_t row;
+};
+
+// a precedes b: larger logit, or equal logit and lower row
+__device__ inline bool precedes(const Entry& a, const Entry& b)
+{
+    return a.key > b.key || (a.key == b.key && a.row < b.row);
+}
+
+// Bitonic sort of n = 2^p entries in LDS, best first (precedes), one entry
+// per thread for the first n threads; every thread of the block calls it.
+template <int N>
+__device__ inline void bitonic_sort(Entry* e)
+{
+    const int tid = threadIdx.x;
+    for (int size = 2; size <= N; size <<= 1) {
+        for (int stride = size / 2; stride > 0; stride >>= 1) {
+            if (tid < N) {
+                const int partner = tid ^ stride;
+                if (partner > tid) {
+                    const bool up = (tid & size) == 0;  // this block sorts best-first
+                    const Entry a = e[tid], b = e[partner];
+                    if (up ? precedes(b, a) : precedes(a, b)) {
+                        e[tid] = b;
+                        e[partner] = a;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+}
+
+// The kk best entries of all V logits into sel[0 .. kk) in any order, by a
+// radix select over the whole array (the path for inputs with so many equal
+// logits that the candidate pool overflows).
+__device__ inline void radix_select_all(const float* __restrict__ logits, int V, int kk, Entry* sel, int* hist,
+                                        int* scan)
+{
+    __shared__ uint32_t s_prefix, s_mask;
+    __shared__ int s_remaining, s_found, s_count;
+    const int tid = threadIdx.x;
+    if (tid == 0) {
+        s_prefix = 0;
+        s_mask = 0;
+        s_remaining = kk;
+        s_count = 0;
+    }
+    __syncthreads();
+    // the kk-th largest key, 11 + 11 + 10 bits from the top
+    constexpr int kShift[3] = {21, 10, 0};
+    constexpr int kBits[3] = {11, 11, 10};
+    int above_total = 0;  // keys strictly above the final prefix (same on all threads)
+#pragma unroll
+    for (int pass = 0; pass < 3; ++pass) {
+        const int bins = 1 << kBits[pass];
+        for (int b = tid; b < 2048; b += kSelectBlock)
+            hist[b] = 0;
+        __syncthreads();
+        const uint32_t prefix = s_prefix, mask = s_mask;
+        for (int e = tid; e < V; e += kSelectBlock) {
+            const uint32_t key = order_key(logits[e]);
+            if ((key & mask) == prefix)
+                atomicAdd(&hist[(key >> kShift[pass]) & (bins - 1)], 1);
+        }
+        __syncthreads();
+        // thread t owns bins (bins-1-2t, bins-2-2t): the highest bins first
+        const int b_hi = bins - 1 - 2 * tid, b_lo = b_hi - 1;
+        const int c_hi = b_hi >= 0 ? hist[b_hi] : 0;
+        const int c_lo = b_lo >= 0 ? hist[b_lo] : 0;
+        const int incl = block_inclusive_scan(c_hi + c_lo, scan);
+        const int before = incl - c_hi - c_lo;  // keys in higher bins
+        const int remaining = s_remaining;
+        __syncthreads();
+        if (b_hi >= 0 && before < remaining && remaining <= before + c_hi) {
+            s_found = b_hi;
+            s_remaining = remaining - before;
+            scan[0] = before;
+        } else if (b_lo >= 0 && before + c_hi < remaining && remaining <= before + c_hi + c_lo) {
+            s_found = b_lo;
+            s_remaining = remaining - before - c_hi;
+            scan[0] = before + c_hi;
+        }
+        __syncthreads();
+        above_total += scan[0];
+        if (tid == 0) {
+            s_prefix = prefix | ((uint32_t)s_found << kShift[pass]);
+            s_mask = mask | ((uint32_t)(bins - 1) << kShift[pass]);
+        }
+        __syncthreads();
+    }
+    const uint32_t T = s_prefix;      // the kk-th largest key
+    const int need_eq = s_remaining;  // entries equal to T to take, lowest rows first
+    // keys above T: fewer than kk of them, appended in any order
+    for (int e = tid; e < V; e += kSelectBlock) {
+        const uint32_t key = order_key(logits[e]);
+        if (key > T) {
+            const int pos = atomicAdd(&s_count, 1);  // < kk by the selection
+            if (pos < kHeadMaxK)
+                sel[pos] = Entry{key, e};
+        }
+    }
+    // keys equal to T: the need_eq lowest rows, by a scan in row order
+    const int chunk = (V + kSelectBlock - 1) / kSelectBlock;
+    const int e0 = min(V, tid * chunk), e1 = min(V, e0 + chunk);
+    int n_eq = 0;
+    for (int e = e0; e < e1; ++e)
+        n_eq += order_key(logits[e]) == T;
+    const int eq_before = block_inclusive_scan(n_eq, scan) - n_eq;
+    int rank = eq_before;
+    for (int e = e0; e < e1 && rank < need_eq; ++e) {
+        if (order_key(logits[e]) == T) {
+            if (above_total + rank < kHeadMaxK)
+                sel[above_total + rank] = Entry{T, e};
+            ++rank;
+        }
+    }
+    __syncthreads();
+}
+
+template <int CTRL>
+__device__ inline uint32_t max_dpp(uint32_t v)
+{
+    return max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false));
+}
+
+// Maximum over the 64 lanes, in every lane: DPP within each row of 16 lanes,
+// then the four row results read as scalars.
+__device__ inline uint32_t wave_max_u32(uint32_t v)
+{
+    v = max_dpp<0xB1>(v);   // lane ^ 1
+    v = max_dpp<0x4E>(v);   // lane ^ 2
+    v = max_dpp<0x141>(v);  // the other quad of 8
+    v = max_dpp<0x140>(v);  // the other 8 of 16
+    const uint32_t r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+    const uint32_t r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+    return max(max(r0, r1), max(r2, r3));
+}
+
+// Append the lanes' entries with `take` set to the LDS pool: one LDS atomic
+// per wave, positions by lane rank; entries past `cap` are counted, not kept.
+__device__ inline void pool_append(bool take, uint32_t key, int row, Entry* pool, int* count, int cap)
+{
+    const uint64_t m = __ballot(take);
+    if (m == 0)
+        return;
+    const int lane = threadIdx.x % 64;
+    const int first = __ffsll((unsigned long long)m) - 1;
+    int base = 0;
+    if (lane == first)
+        base = atomicAdd(count, __popcll(m));
+    base = __builtin_amdgcn_readlane(base, first);
+    const int pos = base + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+    if (take && pos < cap)
+        pool[pos] = Entry{key, row};
+}
+
+__global__ __launch_bounds__(kSelectBlock) void k_head_select(const float* __restrict__ logits, int V, int top_k,
+                                                              float threshold, const int8_t* __restrict__ Q,
+                                                              const float* __restrict__ scale, int K,
+                                                              const float* __restrict__ x, int32_t* __restrict__ cand,
+                                                              float* __restrict__ cand_logits,
+                                                              int32_t* __restrict__ result)
+{
+    __shared__ Entry pool[kSelectBlock];  // candidates at or above the bound
+    __shared__ Entry sel[kHeadMaxK];
+    __shared__ int hist[2048];
+    __shared__ int scan[kSelectBlock / 64];
+    __shared__ uint32_t wave_low[kSelectBlock / 64];
+    __shared__ int s_pool;
+    __shared__ float rec[kHeadMaxK];
+    __shared__ __align__(16) float xs[kHeadMaxChunks * 256];  // the FP32 activations, for the recompute
+    const int tid = threadIdx.x, lane = tid % 64, w = tid / 64;
+    const int kk = V >= 2 ? max(top_k, 2) : 1;  // entries to select (the gap needs two)
+
+    // A lower bound L on the kk-th largest key: every wave takes the 4
+    // largest of its lanes' maxima (4 distinct elements), and L is the least
+    // of those 64; at least 64 >= kk elements have keys >= L.  Up to
+    // kRegLogits * 1024 logits are read once into registers (every load in
+    // flight together); longer heads are read twice in batches.
+    const bool in_regs = V <= kRegLogits * kSelectBlock;
+    float f[kRegLogits];
+    uint32_t tmax = 0;  // below every finite logit's key
+    if (in_regs) {
+#pragma unroll
+        for (int u = 0; u < kRegLogits; ++u) {
+            const int e = tid + u * kSelectBlock;
+            f[u] = e < V ? logits[e] : __builtin_nanf("");  // NaN: no element (key 0 below)
+        }
+#pragma unroll
+        for (int u = 0; u < kRegLogits; ++u)
+            tmax = max(tmax, tid + u * kSelectBlock < V ? order_key(f[u]) : 0u);
+    } else {
+        for (int e0 = tid; e0 < V; e0 += kScanUnroll * kSelectBlock) {
+            uint32_t g[kScanUnroll];  // all loads of the batch in flight at once
+#pragma unroll
+            for (int u = 0; u < kScanUnroll; ++u) {
+                const int e = e0 + u * kSelectBlock;
+                g[u] = e < V ? order_key(logits[e]) : 0u;
+            }
+#pragma unroll
+            for (int u = 0; u < kScanUnroll; ++u)
+                tmax = max(tmax, g[u]);
+        }
+    }
+    for (int k = tid; k < K; k += kSelectBlock)  // K <= kHeadMaxChunks * 256
+        xs[k] = x[k];
+    uint32_t v = tmax, low = 0xffffffffu;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const uint32_t m = wave_max_u32(v);
+        low = min(low, m);
+        const uint64_t holders = __ballot(v == m);
+        if (lane == __ffsll((unsigned long long)holders) - 1)
+            v = 0;
+    }
+    if (lane == 0)
+        wave_low[w] = low;
+    if (tid == 0)
+        s_pool = 0;
+    __syncthreads();
+    uint32_t L = wave_low[0];
+#pragma unroll
+    for (int i = 1; i < kSelectBlock / 64; ++i)
+        L = min(L, wave_low[i]);
+    L = max(L, 1u);  // key 0 marks "no element"
+    // the pool: every element with key >= L (all of the kk best among them)
+    if (in_regs) {
+#pragma unroll
+        for (int u = 0; u < kRegLogits; ++u) {
+            const int e = tid + u * kSelectBlock;
+            const uint32_t k = e < V ? order_key(f[u]) : 0u;
+            pool_append(k >= L, k, e, pool, &s_pool, kSelectBlock);
+        }
+    } else {
+        for (int e0 = tid; e0 < V; e0 += kScanUnroll * kSelectBlock) {
+            uint32_t g[kScanUnroll];
+#pragma unroll
+            for (int u = 0; u < kScanUnroll; ++u) {
+                const int e = e0 + u * kSelectBlock;
+                g[u] = e < V ? order_key(logits[e]) : 0u;
+            }
+#pragma unroll
+            for (int u = 0; u < kScanUnroll; ++u)
+                pool_append(g[u] >= L, g[u], e0 + u * kSelectBlock, pool, &s_pool, kSelectBlock);
+        }
+    }
+    __syncthreads();
+    const int n_pool = s_pool;
+    if (n_pool <= kSelectBlock) {
+        // the rank of a pooled entry is the number of entries that precede it
+        // (a strict total order), so the kk best land in sel by rank
+        if (tid < n_pool) {
+            const Entry me = pool[tid];
+            int rank = 0;
+            int j = 0;
+            for (; j + 8 <= n_pool; j += 8) {  // eight LDS reads in flight
+                Entry o[8];
+#pragma unroll
+                for (int t = 0; t < 8; ++t)
+                    o[t] = pool[j + t];
+#pragma unroll
+                for (int t = 0; t < 8; ++t)
+                    rank += precedes(o[t], me);
+            }
+            for (; j < n_pool; ++j)
+                rank += precedes(pool[j], me);
+            if (rank < kk)
+                sel[rank] = me;
+        }
+        __syncthreads();
+    } else {
+        // too many equal keys at the bound: select over the whole array
+        __syncthreads();
+        radix_select_all(logits, V, kk, sel, hist, scan);
+        if (tid < kHeadMaxK && tid >= kk)
+            sel[tid] = Entry{0u, 0x7fffffff};
+        __syncthreads();
+        bitonic_sort<kHeadMaxK>(sel);
+    }
+
+    const float l1 = key_value(sel[0].key);
+    const float gap = V >= 2 ? l1 - key_value(sel[1].key) : __builtin_inff();
+    const bool verify = gap < threshold;
+    if (tid < top_k) {
+        cand[tid] = sel[tid].row;
+        if (!verify)
+            cand_logits[tid] = key_value(sel[tid].key);
+    }
+    if (!verify) {
+        if (tid == 0) {
+            result[0] = sel[0].row;
+            result[1] = 0;
+        }
+        return;
+    }
+
+    // Recompute the candidates with the FP32 activations.  Wave w takes
+    // candidates w + 16 r (r < 4); lane l covers bytes 16 l + 1024 c of a row
+    // (c < ceil(K / 1024)); all four rows' weights are loaded before any is
+    // summed, so the 64 rows cost one memory round trip.
+    constexpr int kRowsPerWave = kHeadMaxK / (kSelectBlock / 64);
+    constexpr int kRowsAtOnce = 4;
+    constexpr int kMaxC = kHeadMaxChunks * 256 / 1024;
+    const int n_c = (K + 1023) / 1024;
+    for (int r0 = 0; r0 < kRowsPerWave; r0 += kRowsAtOnce) {
+    u32x4 qd[kRowsAtOnce][kMaxC];
+    float srow[kRowsAtOnce];  // the rows' scales, loaded with their weights
+#pragma unroll
+    for (int r = 0; r < kRowsAtOnce; ++r) {
+        const int i = w + (kSelectBlock / 64) * (r0 + r);
+        srow[r] = i < top_k ? scale[sel[i].row] : 0.0f;
+        const int8_t* qrow = Q + (int64_t)(i < top_k ? sel[i].row : 0) * K;
+#pragma unroll
+        for (int c = 0; c < kMaxC; ++c) {
+            const int k = 16 * lane + 1024 * c;
+            qd[r][c] = (i < top_k && c < n_c && k < K) ? *reinterpret_cast<const u32x4*>(qrow + k)  // Q 16-byte aligned
+                                                        : u32x4{0, 0, 0, 0};
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kRowsAtOnce; ++r) {
+        const int i = w + (kSelectBlock / 64) * (r0 + r);
+        float acc = 0.0f;
+#pragma unroll
+        for (int c = 0; c < kMaxC; ++c) {
+            const int k = 16 * lane + 1024 * c;
+            if (c < n_c && k < K) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const uint32_t d = qd[r][c][t];
+                    const f32x4 x4 = *reinterpret_cast<const f32x4*>(xs + k + 4 * t);
+                    acc = __builtin_fmaf(cvt_i8<0>(d), x4.x, acc);
+                    acc = __builtin_fmaf(cvt_i8<1>(d), x4.y, acc);
+                    acc = __builtin_fmaf(cvt_i8<2>(d), x4.z, acc);
+                    acc = __builtin_fmaf(cvt_i8<3>(d), x4.w, acc);
+                }
+            }
+        }
+#pragma unroll
+        for (int dd = 32; dd >= 1; dd >>= 1)
+            acc += __shfl_xor(acc, dd, 64);
+        if (lane == 0 && i < top_k) {
+            const float res_i = acc * srow[r];
+            rec[i] = res_i;
+            cand_logits[i] = res_i;
+        }
+    }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int best = 0;
+        for (int i = 1; i < top_k; ++i)
+            if (rec[i] > rec[best] || (rec[i] == rec[best] && sel[i].row < sel[best].row))
+                best = i;
+        result[0] = sel[best].row;
+        result[1] = 1;
+    }
+}
+
+}  // namespace spk

@@ -21,7 +21,7 @@ def declared_functions():
     names = set()
     for hdr in glob.glob(os.path.join(ROOT, "include", "*.h")):
         text = re.sub(r"/\*.*?\*/", "", open(hdr).read(), flags=re.S)
-        names |= set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*((?:spike|dense)_\w+)\s*\(", text, flags=re.M))
+        names |= set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*((?:spike|dense|head)_\w+)\s*\(", text, flags=re.M))
     return sorted(names)
 
 
@@ -206,3 +206,20 @@ def test_scale_shape_check_names_the_transposed_export(sp):
     with pytest.raises(sp.SpikeError):
         sp.spike_check_scale_shape(1536, 6144, 0, 1536, 192)
     sp.spike_check_scale_shape(1536, 1536, 32, 1536, 48)  # square: the shapes coincide
+
+
+def test_head_verify_argument_validation_before_any_hip_call(sp):
+    lib = sp.raw_library()
+    d = 0x1000  # never dereferenced: validation fails first
+    f = lib.head_verify_forward
+    assert f(d, d, 24, 100, d, 8, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL  # K % 16
+    assert f(d, d, 4112, 100, d, 8, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL  # K too large
+    assert f(d, d, 1536, 0, d, 8, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL
+    assert f(d, d, 1536, 100, d, 0, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL
+    assert f(d, d, 1536, 100, d, 65, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL
+    assert f(d, d, 1536, 5, d, 6, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL  # top_k > V
+    assert f(d, d, 1536, 100, d, 8, float("nan"), d, d, d, d, None) == sp.SPIKE_EINVAL
+    assert "NaN" in sp.spike_proj_last_error()
+    assert f(d + 4, d, 1536, 100, d, 8, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL
+    assert "16-byte" in sp.spike_proj_last_error()
+    assert f(d, d, 1536, 100, d, 8, 0.5, None, d, d, d, None) == sp.SPIKE_EINVAL
