@@ -172,8 +172,14 @@ def bench_decode_stack(sp, torch, wl, timer, args):
     sec_w = timer(lambda: sp.spike_stream_forward(warm, dmasks, out), max(3, args.steps // 2), 1)
     warm_gbs = step_bytes / sec_w / 1e9
     log(f"stream warm (one weight set, {R}x fewer bytes than the cold copies): {warm_gbs:.1f} GB/s")
-    res = {"sec": sec, "gbs": gbs, "warm_gbs": warm_gbs, "step_bytes": step_bytes, "host": host, "masks": masks,
-           "Ks": Ks}
+    # the same stream summing in exact 16-bit partials (paper Sec. 2.3), for comparison
+    sp.spike_stream_tune(cold, sp.SPIKE_TUNE_SHAPE, sp.SPIKE_SHAPE(*HEADLINE_SHAPE[:4], NT=True, I16=True))
+    sec16 = timer(lambda: sp.spike_stream_forward(cold, dmasks, out), max(3, args.steps // 2), 1)
+    sp.spike_stream_tune(cold, sp.SPIKE_TUNE_SHAPE, sp.SPIKE_SHAPE(*HEADLINE_SHAPE))
+    i16_gbs = step_bytes / sec16 / 1e9
+    log(f"stream cold with 16-bit partial sums: {i16_gbs:.1f} GB/s ({100 * i16_gbs / HBM_PEAK_GBS:.1f}% of HBM)")
+    res = {"sec": sec, "gbs": gbs, "warm_gbs": warm_gbs, "i16_gbs": i16_gbs, "step_bytes": step_bytes,
+           "host": host, "masks": masks, "Ks": Ks}
 
     if not args.no_latency:
         static_mask = torch.zeros(masks.shape[1], dtype=torch.int64, device="cuda")
@@ -645,6 +651,7 @@ def main(argv=None) -> int:
                      "kernel": f"k_stream<Shape{HEADLINE_SHAPE}> (one launch per step)",
                      "kernel_source_hash": kernel_source_hash()},
         "warm_one_set_gbs": round(main_res["warm_gbs"], 1),
+        "int16_partials_cold_gbs": round(main_res["i16_gbs"], 1),
         "per_token_latency": main_res.get("latency"),
         "workloads": extra,
         "cpu_baseline": cpu,

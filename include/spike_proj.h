@@ -194,6 +194,10 @@ int spike_proj_destroy(spike_proj_t h);
 #define SPIKE_TUNE_MFMA_COL_SETS 13
 #define SPIKE_SHAPE(V, LG, U, BLOCK) ((V) | ((LG) << 5) | ((U) << 15) | (((BLOCK) / 64) << 20))
 #define SPIKE_SHAPE_NT (1 << 25) /* or-ed into a shape code: nontemporal weight loads */
+/* or-ed into a shape code: exact 16-bit partial sums (paper Sec. 2.3: bounded
+ * active counts may sum in fewer bits); two channels per register, folded
+ * into INT32 every 256 columns; results are identical */
+#define SPIKE_SHAPE_I16 (1 << 26)
 #define SPIKE_PATH_AUTO 0
 #define SPIKE_PATH_GATHER 1
 #define SPIKE_PATH_MFMA 2

@@ -20,6 +20,7 @@ SPIKE_TUNE_PATH, SPIKE_TUNE_SLICE_WORDS, SPIKE_TUNE_MFMA_MIN_B, SPIKE_TUNE_VEC, 
 SPIKE_TUNE_SHAPE, SPIKE_TUNE_TILES_PER_UNIT, SPIKE_TUNE_XCD_SPREAD, SPIKE_TUNE_MFMA_WAVES = 6, 7, 8, 9
 SPIKE_TUNE_MFMA_DEPTH, SPIKE_TUNE_MFMA_ROW_TILE, SPIKE_TUNE_MFMA_COL_SETS = 11, 12, 13
 SPIKE_SHAPE_NT = 1 << 25
+SPIKE_SHAPE_I16 = 1 << 26
 SPIKE_PATH_AUTO, SPIKE_PATH_GATHER, SPIKE_PATH_MFMA = 0, 1, 2
 SPIKE_DEFAULT_MAX_B = 512
 DENSE_MAX_K, DENSE_MAX_B = 16128, 65535
@@ -28,9 +29,10 @@ DENSE_TUNE_KERNEL, DENSE_TUNE_WG_PER_CU = 1, 2
 SPIKE_LAYOUT_ROW_MAJOR, SPIKE_LAYOUT_COL_MAJOR = 0, 1
 
 
-def SPIKE_SHAPE(V: int, LG: int, U: int, BLOCK: int, NT: bool = False) -> int:
-    """Shape code of the gather launch (same packing as the header macro)."""
-    return V | (LG << 5) | (U << 15) | ((BLOCK // 64) << 20) | (SPIKE_SHAPE_NT if NT else 0)
+def SPIKE_SHAPE(V: int, LG: int, U: int, BLOCK: int, NT: bool = False, I16: bool = False) -> int:
+    """Shape code of the gather launch (same packing as the header macros)."""
+    return (V | (LG << 5) | (U << 15) | ((BLOCK // 64) << 20) | (SPIKE_SHAPE_NT if NT else 0)
+            | (SPIKE_SHAPE_I16 if I16 else 0))
 
 EXPORTED = (
     "spike_proj_create", "spike_proj_reserve", "spike_proj_forward", "spike_proj_forward_acc",

@@ -220,6 +220,42 @@ struct Chunk<1, NT> {  // any N, any alignment
 
 template <int V, bool NT>
 struct BufChunk;
+// Exact lower-width partial sums (paper Sec. 2.3: bounded active counts may
+// sum in fewer bits).  Two channels share a 32-bit register as 16-bit
+// halves holding biased sums: byte b enters as b + 128 in [0, 255], so up
+// to 257 columns sum without overflow, and the bias is removed when the
+// halves are added into the INT32 totals (every at most kI16MaxAdds
+// columns).  Per four weight bytes: one XOR, two byte permutes and two
+// packed 16-bit adds.
+constexpr int kI16MaxAdds = 256;
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// even += (byte 0, byte 2) and odd += (byte 1, byte 3) of d, biased.
+__device__ inline void add_i8x4_i16(uint32_t& even, uint32_t& odd, uint32_t d)
+{
+    const uint32_t u = d ^ 0x80808080u;
+    const uint32_t e = __builtin_amdgcn_perm(0u, u, 0x0c020c00u);  // bytes 0 and 2 into the two halves
+    const uint32_t o = __builtin_amdgcn_perm(0u, u, 0x0c030c01u);  // bytes 1 and 3
+    even = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, even) + __builtin_bit_cast(u16x2, e));
+    odd = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, odd) + __builtin_bit_cast(u16x2, o));
+}
+
+// acc[4i + 0, 2] and acc[4i + 1, 3] take the halves of p[2i] and p[2i + 1]
+// less the bias of n adds; p is cleared.
+__device__ inline void flush_i16(int32_t (&acc)[16], uint32_t (&p)[8], int n)
+{
+    const int32_t bias = 128 * n;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        acc[4 * i + 0] += (int32_t)(p[2 * i] & 0xffffu) - bias;
+        acc[4 * i + 2] += (int32_t)(p[2 * i] >> 16) - bias;
+        acc[4 * i + 1] += (int32_t)(p[2 * i + 1] & 0xffffu) - bias;
+        acc[4 * i + 3] += (int32_t)(p[2 * i + 1] >> 16) - bias;
+        p[2 * i] = 0;
+        p[2 * i + 1] = 0;
+    }
+}
+
 template <bool NT>
 struct BufChunk<16, NT> {
     u32x4 v;
@@ -230,6 +266,13 @@ struct BufChunk<16, NT> {
         add_i8x4(acc + 4, v.y);
         add_i8x4(acc + 8, v.z);
         add_i8x4(acc + 12, v.w);
+    }
+    __device__ void add_i16(uint32_t (&p)[8]) const
+    {
+        add_i8x4_i16(p[0], p[1], v.x);
+        add_i8x4_i16(p[2], p[3], v.y);
+        add_i8x4_i16(p[4], p[5], v.z);
+        add_i8x4_i16(p[6], p[7], v.w);
     }
 };
 template <bool NT>
@@ -258,11 +301,14 @@ struct BufChunk<1, NT> {
 // Launch shape.  Lane groups of LG lanes (a group may span waves); a lane
 // covers V consecutive output channels, a group one tile of TB = LG * V
 // channels of one column at a time; U columns per group are in flight;
-// BLOCK threads per workgroup; NT marks weight loads nontemporal.
-template <int V_, int LG_, int U_, int BLOCK_, bool NT_ = false>
+// BLOCK threads per workgroup; NT marks weight loads nontemporal; I16 sums
+// in exact 16-bit partials (V = 16, buffer-resource kernels).
+template <int V_, int LG_, int U_, int BLOCK_, bool NT_ = false, bool I16_ = false>
 struct Shape {
     static constexpr int V = V_, LG = LG_, U = U_, BLOCK = BLOCK_;
     static constexpr bool NT = NT_;
+    static constexpr bool I16 = I16_;
+    static_assert(!I16 || (V == 16 && kI16MaxAdds % U == 0), "16-bit partials: 16 channels per lane");
     static constexpr int kTile = V * LG;
     static constexpr int kGroups = BLOCK / LG;
     static_assert(BLOCK % LG == 0 && LG >= 1 && LG <= 64 && 64 % LG == 0, "lane groups must tile a wave");
@@ -366,20 +412,53 @@ __device__ inline void gather_ring(__amdgpu_buffer_rsrc_t w, uint32_t N, uint32_
     // The scheduling barriers keep every slot's refill after its add, so a
     // slot's old and new values never live at once (no register copies) and
     // U loads stay in flight; the round's list entries are read first.
-    for (int r = 1; r < rounds; ++r) {
-        uint32_t off[U];
-        offsets(r, off);
+    if constexpr (S::I16) {
+        // 16-bit partials, folded into acc every kI16MaxAdds columns (the
+        // count is per wave: every lane adds U columns, real or zero, per round)
+        uint32_t p16[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        int n16 = 0;
+        for (int r = 1; r < rounds; ++r) {
+            uint32_t off[U];
+            offsets(r, off);
+            if (n16 == kI16MaxAdds) {
+                flush_i16(acc, p16, n16);
+                n16 = 0;
+            }
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            slot[u].add(acc);
-            slot[u].load(w, off[u]);
-            __builtin_amdgcn_sched_barrier(0);
+            for (int u = 0; u < U; ++u) {
+                slot[u].add_i16(p16);
+                slot[u].load(w, off[u]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            n16 += U;
         }
-    }
-    if (rounds > 0) {
+        if (rounds > 0) {
+            if (n16 == kI16MaxAdds) {
+                flush_i16(acc, p16, n16);
+                n16 = 0;
+            }
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-            slot[u].add(acc);
+            for (int u = 0; u < U; ++u)
+                slot[u].add_i16(p16);
+            n16 += U;
+        }
+        flush_i16(acc, p16, n16);
+    } else {
+        for (int r = 1; r < rounds; ++r) {
+            uint32_t off[U];
+            offsets(r, off);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                slot[u].add(acc);
+                slot[u].load(w, off[u]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        if (rounds > 0) {
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                slot[u].add(acc);
+        }
     }
 }
 

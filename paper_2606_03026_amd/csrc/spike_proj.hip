@@ -57,11 +57,11 @@ template <class S, bool BUF>
 void launch_stream_t(const spike_stream* s, int n_tiles, unsigned units, const uint64_t* masks, float* out,
                      hipStream_t st);
 
-template <int V, int LG, int U, int BLOCK, bool NT = false>
+template <int V, int LG, int U, int BLOCK, bool NT = false, bool I16 = false>
 constexpr ShapeEntry entry()
 {
-    using S = spk::Shape<V, LG, U, BLOCK, NT>;
-    return ShapeEntry{SPIKE_SHAPE(V, LG, U, BLOCK) | (NT ? SPIKE_SHAPE_NT : 0),
+    using S = spk::Shape<V, LG, U, BLOCK, NT, I16>;
+    return ShapeEntry{SPIKE_SHAPE(V, LG, U, BLOCK) | (NT ? SPIKE_SHAPE_NT : 0) | (I16 ? SPIKE_SHAPE_I16 : 0),
                       V,
                       LG,
                       U,
@@ -76,6 +76,8 @@ const ShapeEntry kShapes[] = {
     entry<16, 32, 4, 256, true>(), entry<16, 32, 2, 256, true>(), entry<16, 32, 6, 256, true>(),
     entry<16, 32, 8, 256, true>(), entry<16, 32, 4, 512, true>(), entry<16, 64, 4, 256, true>(),
     entry<8, 64, 4, 256, true>(), entry<8, 32, 4, 256, true>(),
+    // exact 16-bit partial sums (buffer-resource kernels; the 64-bit-address ones sum in INT32)
+    entry<16, 32, 4, 256, true, true>(),
     // the same with cached loads (weights re-read soon, e.g. warm caches)
     entry<16, 32, 4, 256>(), entry<8, 64, 4, 256>(),
     // narrow tiles (decode latency)

@@ -503,7 +503,25 @@ def test_errors_on_gpu(sp):
 
 def decode_shape(code):
     return dict(V=code & 31, LG=(code >> 5) & 1023, U=(code >> 15) & 31, BLOCK=((code >> 20) & 31) * 64,
-                NT=bool(code >> 25 & 1))
+                NT=bool(code >> 25 & 1), I16=bool(code >> 26 & 1))
+
+
+@pytest.mark.parametrize("weights", ["min", "max", "random"])
+@pytest.mark.parametrize("p,slice_words", [(1.0, 256), (1.0, 100), (0.6, 256)])
+def test_int16_partials_fold_exactly(sp, weights, p, slice_words):
+    """The 16-bit partial-sum shape over long dense rows: every lane adds
+    thousands of columns, so the biased 16-bit halves are folded into INT32
+    many times, at the extremes of the weight range too."""
+    K, N, B = 16384, 512, 2
+    code = sp.SPIKE_SHAPE(16, 32, 4, 256, NT=True, I16=True)
+    assert code in sp.spike_proj_shapes()
+    q = wl.small_problem(K, N, B, p, seed=11)
+    W = {"min": np.full((K, N), -128, np.int8), "max": np.full((K, N), 127, np.int8), "random": q["W"]}[weights]
+    h, *_ = make(sp, W, q["scale"])
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_PATH, sp.SPIKE_PATH_GATHER)
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_SHAPE, code)
+    sp.spike_proj_tune(h, sp.SPIKE_TUNE_SLICE_WORDS, slice_words)
+    assert_parity(sp, h, W, q["scale"], q["masks"], threads=16)
 
 
 @pytest.mark.parametrize("K,N", [(1536, 1536), (6144, 1536), (333, 1000), (70, 96)])
