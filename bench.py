@@ -377,17 +377,21 @@ def write_traffic_record(fetch_csv: str, write_csv: str, steps: int, warmup: int
     """Assemble the HBM-traffic record of the headline stream kernel from two
     rocprofv3 --pmc runs of `bench.py --only-stream --copy-probe` (one with
     FETCH_SIZE, one with WRITE_SIZE; KiB per dispatch).  Each counter is
-    scaled by what it reads for the 1 GiB copy of --copy-probe.  The first
-    warmup + steps stream dispatches are the cold (rotated-copies) ones."""
+    scaled by what it reads for the 1 GiB copy of --copy-probe.  Of the
+    headline shape's stream dispatches, the first warmup + steps are the cold
+    (rotated-copies) ones and the rest the warm (one weight set) ones."""
     import csv
     from paper_2606_03026_amd import workloads as wl
+
+    V, LG, U, BLOCK, NT = HEADLINE_SHAPE
+    headline = f"spk::k_stream<spk::Shape<{V}, {LG}, {U}, {BLOCK}, {str(NT).lower()}, false>"
 
     def rows(path, counter):
         out = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
         out.sort(key=lambda r: int(r["Dispatch_Id"]))
         copy = max((r for r in out if r["Kernel_Name"].startswith("__amd_rocclr_copyBuffer")),
                    key=lambda r: float(r["Counter_Value"]))
-        stream = [float(r["Counter_Value"]) for r in out if "spk::k_stream<" in r["Kernel_Name"]]
+        stream = [float(r["Counter_Value"]) for r in out if headline in r["Kernel_Name"]]
         return float(copy["Counter_Value"]), stream
 
     gib_kib = float(1 << 20)
