@@ -132,7 +132,9 @@ inline int mfma_lds_bytes(int RT, int CS, int wpr)
 // One output tile (tile id `id` of the launch's n_rowtiles x n_coltiles
 // tiles) of one projection.
 template <int RT, int CS, int KW, int D, bool PRELOAD, bool ACC>
-__device__ inline void mfma_tile(const int8_t* __restrict__ P, const float* __restrict__ scale, int N,
+// Always inlined: as a called function it spills (the call ABI) and runs
+// several times slower.
+__device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __restrict__ P, const float* __restrict__ scale, int N,
                                  const uint64_t* __restrict__ mask, int wpr, int B, int n_rowtiles, int n_coltiles,
                                  int id, float* __restrict__ out, int32_t* __restrict__ acc_out)
 {
@@ -170,17 +172,36 @@ __device__ inline void mfma_tile(const int8_t* __restrict__ P, const float* __re
                                                           ((t0 + t) * wpr + s) * kMfmaSetStepBytes, 0);
     };
 
-    // The output entries of this thread (see the final loop) and, for FP32
-    // outputs, their scales, loaded now so that the epilogue does not wait
-    // for them.
+    // Output form (see the final loops).  Tall tiles (RT >= 4: batches of
+    // more than 64 rows), where N and the output (and scale) addresses allow
+    // it, write four consecutive channels of one row per thread with one
+    // 16-byte store (quad e4 = entries 4 e4 .. 4 e4 + 3 of the partial tile);
+    // otherwise one channel per thread and entry.  Either way the scales are
+    // loaded now, so that the epilogue does not wait for them.
     constexpr int kPer = (RED + BLOCK - 1) / BLOCK;
-    float sc[kPer];
+    constexpr int kPer4 = (RED / 4 + BLOCK - 1) / BLOCK;
+    const uintptr_t dst_addr = ACC ? reinterpret_cast<uintptr_t>(acc_out) : reinterpret_cast<uintptr_t>(out);
+    const uintptr_t sc_addr = ACC ? 0 : reinterpret_cast<uintptr_t>(scale);
+    const bool vec_out = RT >= 4 && N % 4 == 0 && ((dst_addr | sc_addr) & 15) == 0;
+    f32x4 sc4[RT >= 4 ? kPer4 : 1];
+    float sc[RT >= 4 ? 1 : kPer];
     if constexpr (!ACC) {
+        if constexpr (RT >= 4) {
 #pragma unroll
-        for (int r = 0; r < kPer; ++r) {
-            const int e = threadIdx.x + r * BLOCK;
-            const int t = (e / 256) % CS;
-            sc[r] = e < RED ? scale[16 * (t0 + t) + e % 16] : 0.0f;
+            for (int r = 0; r < kPer4; ++r) {
+                const int e4 = threadIdx.x + r * BLOCK;
+                const int t = (e4 / 64) % CS;
+                sc4[r] = vec_out && e4 < RED / 4
+                             ? *reinterpret_cast<const f32x4*>(scale + 16 * (t0 + t) + 4 * (e4 % 4))
+                             : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            }
+        } else {
+#pragma unroll
+            for (int r = 0; r < kPer; ++r) {
+                const int e = threadIdx.x + r * BLOCK;
+                const int t = (e / 256) % CS;
+                sc[r] = e < RED ? scale[16 * (t0 + t) + e % 16] : 0.0f;
+            }
         }
     }
 
@@ -311,6 +332,36 @@ __device__ inline void mfma_tile(const int8_t* __restrict__ P, const float* __re
     __syncthreads();
 
     // entry e -> row m0 + 16 ms + 4 (lane / 16) + j, channel 16 (t0 + t) + lane % 16
+    if constexpr (RT >= 4) if (vec_out) {
+        // quad e4 -> entries 4 e4 .. 4 e4 + 3: block g = e4 / 16 of 64
+        // entries, lanes 4 (e4 % 16) .. + 3, i.e. one row, four channels
+#pragma unroll
+        for (int r = 0; r < kPer4; ++r) {
+            const int e4 = threadIdx.x + r * BLOCK;
+            if (e4 >= RED / 4)
+                break;
+            const int g = e4 / 16, qd = e4 % 16;
+            const int j = g % 4, mt = g / 4;
+            const int ms = mt / CS, t = mt % CS;
+            const int b = m0 + 16 * ms + 4 * (qd / 4) + j;
+            if (b >= B)
+                continue;
+            const int64_t n0 = 16 * (t0 + t) + 4 * (qd % 4);
+            const i32x4 sum = *reinterpret_cast<const i32x4*>(red + 4 * e4);
+            if constexpr (ACC) {
+                *reinterpret_cast<i32x4*>(acc_out + (int64_t)b * N + n0) = sum;
+            } else {
+                const f32x4 s4 = sc4[r];
+                f32x4 y;  // exact for |sum| < 2^24, RNE beyond; one binary32 multiply each
+                y.x = (float)sum.x * s4.x;
+                y.y = (float)sum.y * s4.y;
+                y.z = (float)sum.z * s4.z;
+                y.w = (float)sum.w * s4.w;
+                __builtin_nontemporal_store(y, reinterpret_cast<f32x4*>(out + (int64_t)b * N + n0));
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int r = 0; r < kPer; ++r) {
         const int e = threadIdx.x + r * BLOCK;
@@ -328,7 +379,7 @@ __device__ inline void mfma_tile(const int8_t* __restrict__ P, const float* __re
             acc_out[(int64_t)b * N + n] = sum;
         } else {
             const float as_float = (float)sum;  // exact for |sum| < 2^24, RNE beyond
-            out[(int64_t)b * N + n] = as_float * sc[r];
+            out[(int64_t)b * N + n] = as_float * (RT >= 4 ? scale[n] : sc[RT >= 4 ? 0 : r]);
         }
     }
 }
