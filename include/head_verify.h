@@ -38,9 +38,17 @@
  *   cand_logits  float [top_k] out: the recomputed logits when verification
  *                ran, else the candidates' approximate logits.
  *   result       int32 [2] out: {token, 1 if verification ran else 0}.
+ *   workspace    device memory of head_verify_workspace_bytes() bytes,
+ *                16-byte aligned, owned by the caller; no initial contents
+ *                are needed and nothing in it outlives the call.  Calls that
+ *                share a workspace must not overlap: enqueue them on one
+ *                stream, or give each stream its own workspace.
  * Two kernels are enqueued on `stream` (a hipStream_t, NULL for the default
- * stream); the gate is decided on the device, so the call never waits for
- * the GPU and can be captured in a HIP graph.  Nothing is allocated.
+ * stream): the approximate head, which also recomputes a few likely
+ * candidates ahead of the gate when threshold > 0, and the selection, gate
+ * and verification.  The gate is decided on the device, so the call never
+ * waits for the GPU and can be captured in a HIP graph.  Nothing is
+ * allocated.
  *
  * Errors: SPIKE_OK (0) or a negative code from spike_proj.h, with the
  * message in spike_proj_last_error(); arguments are validated before any
@@ -60,9 +68,12 @@ extern "C" {
 #define HEAD_MAX_TOP_K 64
 #define HEAD_MAX_K 4096
 
+/* Bytes of the workspace head_verify_forward needs (the same for every V). */
+int64_t head_verify_workspace_bytes(void);
+
 int head_verify_forward(const int8_t *Q, const float *scale, int32_t K, int32_t V, const float *x, int32_t top_k,
                         float threshold, float *logits, int32_t *cand, float *cand_logits, int32_t *result,
-                        void *stream);
+                        void *workspace, void *stream);
 
 #ifdef __cplusplus
 }

@@ -41,7 +41,7 @@ EXPORTED = (
     "spike_proj_last_error", "spike_proj_shapes", "spike_mfma_plans", "spike_proj_plan_query",
     "spike_proj_abi_version", "spike_proj_forward_noalloc", "spike_proj_create_reserved",
     "spike_stack_forward_fused", "dense_proj_forward", "dense_proj_plan", "dense_proj_tune",
-    "spike_quantize_int8", "spike_check_scale_shape", "head_verify_forward",
+    "spike_quantize_int8", "spike_check_scale_shape", "head_verify_forward", "head_verify_workspace_bytes",
 )
 
 if not os.path.exists(LIB):
@@ -74,13 +74,15 @@ _sig = {
     "dense_proj_tune": [_i32, _i32],
     "spike_quantize_int8": [_p, _i32, _i32, _i32, _p, _p, _p],
     "spike_check_scale_shape": [_i32, _i32, _i32, _i32, _i32],
-    "head_verify_forward": [_p, _p, _i32, _i32, _p, _i32, ctypes.c_float, _p, _p, _p, _p, _p],
+    "head_verify_forward": [_p, _p, _i32, _i32, _p, _i32, ctypes.c_float, _p, _p, _p, _p, _p, _p],
+    "head_verify_workspace_bytes": [],
 }
 for _name, _args in _sig.items():
     getattr(_lib, _name).argtypes = _args
     getattr(_lib, _name).restype = ctypes.c_int
 _lib.spike_proj_last_error.argtypes = []
 _lib.spike_proj_last_error.restype = ctypes.c_char_p
+_lib.head_verify_workspace_bytes.restype = ctypes.c_int64
 
 
 class SpikeError(RuntimeError):
@@ -362,10 +364,21 @@ def spike_check_scale_shape(M: int, K: int, group: int, scale_rows: int, scale_c
            "spike_check_scale_shape")
 
 
+def head_verify_workspace(device=None) -> torch.Tensor:
+    """A workspace for head_verify_forward on `device` (head_verify.h)."""
+    n = int(_lib.head_verify_workspace_bytes())
+    return torch.empty(n, dtype=torch.uint8, device=device if device is not None else "cuda")
+
+
+_head_workspaces: dict = {}
+
+
 def head_verify_forward(Q: torch.Tensor, scale: torch.Tensor, x: torch.Tensor, top_k: int, threshold: float,
                         logits: torch.Tensor, cand: torch.Tensor, cand_logits: torch.Tensor, result: torch.Tensor,
-                        stream=None) -> None:
-    """INT8-activation head, top-k candidates, gap gate, FP32 recompute (head_verify.h)."""
+                        stream=None, workspace: torch.Tensor | None = None) -> None:
+    """INT8-activation head, top-k candidates, gap gate, FP32 recompute
+    (head_verify.h).  Without `workspace`, one kept per device is used (calls
+    on several streams of one device then need their own)."""
     if Q.dtype != torch.int8 or Q.dim() != 2:
         raise TypeError("Q must be a 2-D int8 tensor [V][K]")
     V, K = Q.shape
@@ -375,10 +388,17 @@ def head_verify_forward(Q: torch.Tensor, scale: torch.Tensor, x: torch.Tensor, t
         if t.dtype != dt:
             raise TypeError(f"{name} must be {dt}")
     k = int(top_k)
+    if workspace is None:
+        dev = Q.device.index if Q.device.index is not None else torch.cuda.current_device()
+        workspace = _head_workspaces.get(dev)
+        if workspace is None:
+            workspace = _head_workspaces[dev] = head_verify_workspace(torch.device("cuda", dev))
+    n_ws = int(_lib.head_verify_workspace_bytes())
     _check(_lib.head_verify_forward(_dev_ptr(Q, "Q"), _dev_ptr(scale, "scale", V * 4), int(K), int(V),
                                     _dev_ptr(x, "x", K * 4), k, float(threshold), _dev_ptr(logits, "logits", V * 4),
                                     _dev_ptr(cand, "cand", k * 4), _dev_ptr(cand_logits, "cand_logits", k * 4),
-                                    _dev_ptr(result, "result", 8), _stream(stream)), "head_verify_forward")
+                                    _dev_ptr(result, "result", 8), _dev_ptr(workspace, "workspace", n_ws),
+                                    _stream(stream)), "head_verify_forward")
 
 
 def spike_proj_abi_version() -> int:

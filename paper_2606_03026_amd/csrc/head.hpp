@@ -15,17 +15,29 @@
 // U rows of 16-byte weight loads in flight, rows q + Gq r per lane group,
 // results parked in lanes and stored 32 rows at a time.
 //
-// k_head_select: one workgroup of 1024 threads.  Finds the KK = max(K, 2)
-// largest logits on order-preserving 32-bit keys: a lower bound L on the
-// KK-th largest comes from the threads' maxima, the elements at or above L
-// (typically one to a few hundred) are pooled in LDS and each is placed by
-// its rank among them (equal logits by ascending row); when ties push the
-// pool past 1024 entries, a radix select over the whole array (digits of
-// 11, 11 and 10 bits, LDS histograms) picks the KK instead.  It then computes
-// the gap fl32(l(1) - l(2)) and, when it is below the threshold, recomputes
-// the K candidate rows with the FP32 activations (one wave per row: per
-// lane an FMA chain over its 16-byte chunks, a 6-level lane tree, one
-// multiply by s_m) and picks the largest (ties: the lower row).
+// At the end of k_head_approx each workgroup lists its four largest logits
+// and the largest key it leaves out; when the gate can ask for verification
+// (threshold > 0), its four waves also recompute the four listed rows with
+// the FP32 activations right away, while the approximate head still runs.
+//
+// k_head_select: one workgroup of 1024 threads.  The KK = max(K, 2) largest
+// logits are found on order-preserving 32-bit keys: a lower bound L on the
+// KK-th largest comes from the workgroup maxima, the listed entries at or
+// above L (typically about a hundred) are pooled in LDS and each is placed by
+// its rank among them (equal logits by ascending row).  The lists suffice
+// when every key they leave out is below the KK-th selected key; otherwise
+// the whole array is scanned (pooling, or past 1024 entries a radix select
+// with digits of 11, 11 and 10 bits).  It then computes the gap
+// fl32(l(1) - l(2)) and, when it is below the threshold, takes the K
+// candidates' recomputed logits (per lane an FMA chain over its 16-byte
+// chunks, a 6-level lane tree, one multiply by s_m) from the lists, or
+// computes them itself after a whole-array selection, and picks the largest
+// (ties: the lower row).
+//
+// Reading the 57,344 logits, or the 64 candidate rows, from memory in one
+// workgroup is bound by the misses one compute unit keeps in flight; the
+// lists cut the first to 20 KB and the speculative recompute spreads the
+// second over the approximate head's workgroups.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -37,10 +49,9 @@
 namespace spk {
 
 constexpr int kHeadMaxK = 64;          // candidates
-constexpr int kSelectBlock = 1024;
-constexpr int kScanUnroll = 16;        // logits loaded per thread before any is used
-constexpr int kRegLogits = 56;         // heads up to 56 * 1024 = 57,344 rows are read into registers once
+constexpr int kSelectBlock = 1024;     // threads of a selecting workgroup
 constexpr int kHeadMaxChunks = 16;     // K <= 16 * 256 = 4096 in the recompute
+constexpr int kListLen = 4;            // largest logits each approximate-head workgroup lists
 
 template <int CTRL>
 __device__ inline int add_dpp_int(int v)
@@ -83,12 +94,93 @@ __device__ inline float activation_scale(const float* __restrict__ x, int K, flo
     return __fdiv_rn(fmaxf(m, 1e-8f), 127.0f);
 }
 
-template <int NPL, int U>
+// Order-preserving key of a float: larger floats give larger keys.
+__device__ inline uint32_t order_key(float f)
+{
+    const uint32_t u = __builtin_bit_cast(uint32_t, f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ inline float key_value(uint32_t k)
+{
+    const uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+    return __builtin_bit_cast(float, u);
+}
+
+template <int CTRL>
+__device__ inline uint32_t max_dpp(uint32_t v)
+{
+    return max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false));
+}
+
+// Maximum over the 64 lanes, in every lane: DPP within each row of 16 lanes,
+// then the four row results read as scalars.
+__device__ inline uint32_t wave_max_u32(uint32_t v)
+{
+    v = max_dpp<0xB1>(v);   // lane ^ 1
+    v = max_dpp<0x4E>(v);   // lane ^ 2
+    v = max_dpp<0x141>(v);  // the other quad of 8
+    v = max_dpp<0x140>(v);  // the other 8 of 16
+    const uint32_t r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+    const uint32_t r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+    return max(max(r0, r1), max(r2, r3));
+}
+
+// FP32 logit of one row with the FP32 activations, computed by one wave:
+// lane l covers bytes 16 l + 1024 c of the row (c < ceil(K / 1024)), all
+// loaded at once; a per-lane FMA chain over its chunks, a 6-level lane tree
+// and one multiply by the row's scale.  Every lane returns the result.
+__device__ inline float recompute_row(const int8_t* __restrict__ Q, const float* __restrict__ scale, int K,
+                                      const float* __restrict__ x, int row)
+{
+    constexpr int kMaxC = kHeadMaxChunks * 256 / 1024;
+    const int lane = threadIdx.x % 64;
+    const int n_c = (K + 1023) / 1024;
+    const int8_t* qrow = Q + (int64_t)row * K;
+    u32x4 qd[kMaxC];
+    f32x4 xv[kMaxC][4];
+#pragma unroll
+    for (int c = 0; c < kMaxC; ++c) {
+        const int k = 16 * lane + 1024 * c;
+        const bool ok = c < n_c && k < K;
+        qd[c] = ok ? *reinterpret_cast<const u32x4*>(qrow + k) : u32x4{0, 0, 0, 0};  // Q 16-byte aligned
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            xv[c][t] = ok ? f32x4{x[k + 4 * t], x[k + 4 * t + 1], x[k + 4 * t + 2], x[k + 4 * t + 3]}
+                          : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    const float s = scale[row];
+    float acc = 0.0f;
+#pragma unroll
+    for (int c = 0; c < kMaxC; ++c) {
+        const int k = 16 * lane + 1024 * c;
+        if (c < n_c && k < K) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const uint32_t d = qd[c][t];
+                acc = __builtin_fmaf(cvt_i8<0>(d), xv[c][t].x, acc);
+                acc = __builtin_fmaf(cvt_i8<1>(d), xv[c][t].y, acc);
+                acc = __builtin_fmaf(cvt_i8<2>(d), xv[c][t].z, acc);
+                acc = __builtin_fmaf(cvt_i8<3>(d), xv[c][t].w, acc);
+            }
+        }
+    }
+#pragma unroll
+    for (int dd = 32; dd >= 1; dd >>= 1)
+        acc += __shfl_xor(acc, dd, 64);
+    return acc * s;
+}
+
+template <int NPL, int U, bool SPEC>
 __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restrict__ Q, const float* __restrict__ scale,
                                                            int K, int V, const float* __restrict__ x,
-                                                           float* __restrict__ logits)
+                                                           float* __restrict__ logits, uint64_t* __restrict__ lists,
+                                                           float* __restrict__ list_rec)
 {
     __shared__ float red[kRegBlock / 64];
+    __shared__ uint64_t wave_best[kRegBlock / 64][kListLen];
+    __shared__ uint32_t wave_next[kRegBlock / 64];
+    __shared__ __align__(16) int8_t xq_lds[kHeadMaxChunks * 256];  // the quantized activations
     const int l = threadIdx.x % kRegLanes;
     const int q = blockIdx.x * kRegGroups + threadIdx.x / kRegLanes;
     const int Gq = gridDim.x * kRegGroups;
@@ -119,21 +211,19 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
             slot[u][j] = __builtin_amdgcn_raw_buffer_load_b128(qres, base + chunk_off[j], 0, 2);
     }
     const float sx = activation_scale<kRegBlock>(x, K, red);
-    // this lane's activations as packed INT8 (zeros past K)
+    // the vector quantized once per workgroup (each element by one thread),
+    // then this lane's activations as packed INT8 (zeros past K)
+    for (int k = threadIdx.x; k < K; k += kRegBlock)
+        xq_lds[k] = quant_act(x[k], sx);
+    __syncthreads();
     uint32_t xq[NPL][4];
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
         const int c = l + kRegLanes * j;
+        const u32x4 v = c < n_chunks ? *reinterpret_cast<const u32x4*>(xq_lds + 16 * c) : u32x4{0, 0, 0, 0};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            uint32_t packed = 0;
-            if (c < n_chunks) {
-#pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    packed |= (uint32_t)(uint8_t)quant_act(x[c * 16 + 4 * i + t], sx) << (8 * t);
-            }
-            xq[j][i] = packed;
-        }
+        for (int i = 0; i < 4; ++i)
+            xq[j][i] = v[i];
     }
     auto scale_of_step = [&](int rr) -> float {
         const int m = q + Gq * rr;
@@ -142,6 +232,9 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
     };
     float sc = scale_of_step(l);
     int parked = 0;
+    // this lane's five largest stored logits, largest first (key 0: none)
+    uint32_t tk[kListLen + 1] = {};
+    int trow[kListLen + 1] = {};
     for (int r0 = 0; r0 < n_steps; r0 += U) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -167,25 +260,94 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
                 const int m = q + Gq * rr;
                 if (rr <= r && m < V) {
                     const float c = sc * sx;
-                    logits[m] = (float)parked * c;
+                    const float lg = (float)parked * c;
+                    logits[m] = lg;
+                    uint32_t ck = order_key(lg);
+                    int cr = m;
+#pragma unroll
+                    for (int i = 0; i <= kListLen; ++i) {  // insertion, larger keys first
+                        const bool up = ck > tk[i];
+                        const uint32_t ok = tk[i];
+                        const int orow = trow[i];
+                        tk[i] = up ? ck : ok;
+                        trow[i] = up ? cr : orow;
+                        ck = up ? ok : ck;
+                        cr = up ? orow : cr;
+                    }
                 }
                 sc = scale_of_step((r & ~31) + 32 + l);
             }
         }
     }
-}
-
-// Order-preserving key of a float: larger floats give larger keys.
-__device__ inline uint32_t order_key(float f)
-{
-    const uint32_t u = __builtin_bit_cast(uint32_t, f);
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
-__device__ inline float key_value(uint32_t k)
-{
-    const uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
-    return __builtin_bit_cast(float, u);
+    // The workgroup's four largest logits and the largest key it leaves out:
+    // each wave pops its lanes' heads five times, then wave 0 merges the
+    // waves' entries the same way.  The selection takes the candidates from
+    // these lists.  With SPEC (a gate that can ask for verification), wave w
+    // also recomputes listed row w with the FP32 activations.
+    static_assert(kRegBlock / 64 == kListLen, "one listed row per wave");
+    __shared__ int final_row[kListLen];
+    __shared__ uint32_t final_key[kListLen];
+    const int lane64 = threadIdx.x % 64, wv = threadIdx.x / 64;
+    uint64_t best[kListLen];
+    uint32_t next = 0;
+#pragma unroll
+    for (int r = 0; r <= kListLen; ++r) {
+        const uint32_t m = wave_max_u32(tk[0]);
+        const int h = __ffsll((unsigned long long)__ballot(tk[0] == m)) - 1;
+        const int hrow = __builtin_amdgcn_readlane(trow[0], h);
+        if (r < kListLen)
+            best[r] = (uint64_t)m << 32 | (uint32_t)hrow;
+        else
+            next = m;
+        if (lane64 == h) {
+#pragma unroll
+            for (int i = 0; i < kListLen; ++i) {
+                tk[i] = tk[i + 1];
+                trow[i] = trow[i + 1];
+            }
+            tk[kListLen] = 0;
+        }
+    }
+    if (lane64 == 0) {
+#pragma unroll
+        for (int r = 0; r < kListLen; ++r)
+            wave_best[wv][r] = best[r];
+        wave_next[wv] = next;
+    }
+    __syncthreads();
+    uint64_t* my_list = lists + (int64_t)blockIdx.x * (kListLen + 1);
+    if (wv == 0) {
+        const uint64_t e = lane64 < (kRegBlock / 64) * kListLen ? wave_best[lane64 / kListLen][lane64 % kListLen] : 0ull;
+        uint32_t ek = (uint32_t)(e >> 32);
+        uint32_t nx = wave_max_u32(lane64 < kRegBlock / 64 ? wave_next[lane64] : 0u);
+#pragma unroll
+        for (int r = 0; r <= kListLen; ++r) {
+            const uint32_t m = wave_max_u32(ek);
+            const int h = __ffsll((unsigned long long)__ballot(ek == m)) - 1;
+            if (r < kListLen) {
+                const uint32_t row = __builtin_amdgcn_readlane((uint32_t)e, h);
+                if (lane64 == 0) {
+                    my_list[r] = (uint64_t)m << 32 | row;
+                    final_row[r] = (int)row;
+                    final_key[r] = m;
+                }
+            } else {
+                nx = max(nx, m);
+            }
+            if (lane64 == h)
+                ek = 0;
+        }
+        if (lane64 == 0)
+            my_list[kListLen] = (uint64_t)nx << 32;
+    }
+    if constexpr (SPEC) {
+        __syncthreads();
+        if (final_key[wv] != 0) {
+            const float r = recompute_row(Q, scale, K, x, final_row[wv]);
+            if (lane64 == 0)
+                list_rec[(int64_t)blockIdx.x * kListLen + wv] = r;
+        }
+    }
 }
 
 // Inclusive prefix sum over the 1024 threads of the workgroup (scan[] holds
@@ -331,28 +493,12 @@ __device__ inline void radix_select_all(const float* __restrict__ logits, int V,
     __syncthreads();
 }
 
-template <int CTRL>
-__device__ inline uint32_t max_dpp(uint32_t v)
-{
-    return max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false));
-}
-
-// Maximum over the 64 lanes, in every lane: DPP within each row of 16 lanes,
-// then the four row results read as scalars.
-__device__ inline uint32_t wave_max_u32(uint32_t v)
-{
-    v = max_dpp<0xB1>(v);   // lane ^ 1
-    v = max_dpp<0x4E>(v);   // lane ^ 2
-    v = max_dpp<0x141>(v);  // the other quad of 8
-    v = max_dpp<0x140>(v);  // the other 8 of 16
-    const uint32_t r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
-    const uint32_t r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
-    return max(max(r0, r1), max(r2, r3));
-}
 
 // Append the lanes' entries with `take` set to the LDS pool: one LDS atomic
 // per wave, positions by lane rank; entries past `cap` are counted, not kept.
-__device__ inline void pool_append(bool take, uint32_t key, int row, Entry* pool, int* count, int cap)
+// With `vals`, each entry's value goes to the same position there.
+__device__ inline void pool_append(bool take, uint32_t key, int row, Entry* pool, int* count, int cap,
+                                   float val = 0.0f, float* vals = nullptr)
 {
     const uint64_t m = __ballot(take);
     if (m == 0)
@@ -364,46 +510,146 @@ __device__ inline void pool_append(bool take, uint32_t key, int row, Entry* pool
         base = atomicAdd(count, __popcll(m));
     base = __builtin_amdgcn_readlane(base, first);
     const int pos = base + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
-    if (take && pos < cap)
+    if (take && pos < cap) {
         pool[pos] = Entry{key, row};
+        if (vals)
+            vals[pos] = val;
+    }
 }
 
+// Device workspace of one head verification: written by the approximate
+// head, read by the selection of the same call (no state across calls).
+constexpr int kApproxMaxWgs = 512;   // the approximate head's grid is at most this
+constexpr int kScanUnroll = 16;      // logits per thread loaded before any is used (full scan)
+constexpr int kMergeCap = 1024;      // pooled entries the selection ranks in LDS
+struct HeadWorkspace {
+    // per approximate-head workgroup: its kListLen largest logits (key << 32 |
+    // row, largest first, key 0: none), then the largest key it does not list
+    uint64_t lists[kApproxMaxWgs][kListLen + 1];
+    // the listed rows recomputed with the FP32 activations (when the gate can
+    // ask for verification)
+    float list_rec[kApproxMaxWgs][kListLen];
+};
+
+// Rank selection of the kk best of n pooled entries into sel: the rank of
+// an entry is the number of entries that precede it (a strict total order).
+__device__ inline void rank_pool(const Entry* pool, int n, int kk, Entry* sel, const float* vals = nullptr,
+                                 float* sel_vals = nullptr)
+{
+    const int tid = threadIdx.x;
+    if (tid < n) {
+        const Entry me = pool[tid];
+        int rank = 0;
+        int j = 0;
+        for (; j + 8 <= n; j += 8) {  // eight LDS reads in flight
+            Entry o[8];
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+                o[t] = pool[j + t];
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+                rank += precedes(o[t], me);
+        }
+        for (; j < n; ++j)
+            rank += precedes(pool[j], me);
+        if (rank < kk) {
+            sel[rank] = me;
+            if (vals)
+                sel_vals[rank] = vals[tid];
+        }
+    }
+    __syncthreads();
+}
+
+// Candidate selection, gate and verification, one workgroup.  The
+// approximate head left, per workgroup, its four largest logits, the largest
+// key it did not list, and (SPEC) the listed rows recomputed with the FP32
+// activations.  A lower bound L on the kk-th largest key: every wave takes
+// the 4 largest workgroup maxima it holds (distinct elements) and L is the
+// least of those 64, so at least 64 >= kk elements have keys >= L.  The
+// listed entries at or above L are pooled and ranked; the result is exact
+// when every key left out of the lists is below the kk-th selected key.
+// Otherwise (many equal or clustered logits) the whole array is scanned:
+// elements at or above L are pooled and ranked, or, past 1024 of them, a
+// radix select picks the kk.  Then the gap and the gate; when verification
+// runs, the candidates' recomputed logits come from the lists, or, after a
+// whole-array selection, are computed here (one wave per row), and the token
+// is the largest (ties: the lower row).
 __global__ __launch_bounds__(kSelectBlock) void k_head_select(const float* __restrict__ logits, int V, int top_k,
-                                                              float threshold, const int8_t* __restrict__ Q,
+                                                              float threshold, int n_approx, int spec,
+                                                              const HeadWorkspace* __restrict__ ws,
+                                                              const int8_t* __restrict__ Q,
                                                               const float* __restrict__ scale, int K,
-                                                              const float* __restrict__ x, int32_t* __restrict__ cand,
+                                                              const float* __restrict__ x,
+                                                              int32_t* __restrict__ cand,
                                                               float* __restrict__ cand_logits,
                                                               int32_t* __restrict__ result)
 {
-    __shared__ Entry pool[kSelectBlock];  // candidates at or above the bound
+    __shared__ Entry pool[kMergeCap];
+    __shared__ float pool_rec[kMergeCap];
     __shared__ Entry sel[kHeadMaxK];
+    __shared__ float sel_rec[kHeadMaxK];
     __shared__ int hist[2048];
     __shared__ int scan[kSelectBlock / 64];
-    __shared__ uint32_t wave_low[kSelectBlock / 64];
-    __shared__ int s_pool;
-    __shared__ float rec[kHeadMaxK];
-    __shared__ __align__(16) float xs[kHeadMaxChunks * 256];  // the FP32 activations, for the recompute
+    __shared__ uint32_t wave_low[kSelectBlock / 64], wave_next[kSelectBlock / 64];
+    __shared__ int s_count;
     const int tid = threadIdx.x, lane = tid % 64, w = tid / 64;
     const int kk = V >= 2 ? max(top_k, 2) : 1;  // entries to select (the gap needs two)
 
-    // A lower bound L on the kk-th largest key: every wave takes the 4
-    // largest of its lanes' maxima (4 distinct elements), and L is the least
-    // of those 64; at least 64 >= kk elements have keys >= L.  Up to
-    // kRegLogits * 1024 logits are read once into registers (every load in
-    // flight together); longer heads are read twice in batches.
-    const bool in_regs = V <= kRegLogits * kSelectBlock;
-    float f[kRegLogits];
-    uint32_t tmax = 0;  // below every finite logit's key
-    if (in_regs) {
+    // this thread's workgroup list (spread so that each wave holds
+    // ceil(n_approx / 16) of them), all loads at once
+    const int b = lane * (kSelectBlock / 64) + w;
+    uint64_t ent[kListLen + 1];
+    float erec[kListLen];
 #pragma unroll
-        for (int u = 0; u < kRegLogits; ++u) {
-            const int e = tid + u * kSelectBlock;
-            f[u] = e < V ? logits[e] : __builtin_nanf("");  // NaN: no element (key 0 below)
-        }
+    for (int i = 0; i <= kListLen; ++i)
+        ent[i] = b < n_approx ? ws->lists[b][i] : 0ull;
 #pragma unroll
-        for (int u = 0; u < kRegLogits; ++u)
-            tmax = max(tmax, tid + u * kSelectBlock < V ? order_key(f[u]) : 0u);
-    } else {
+    for (int i = 0; i < kListLen; ++i)
+        erec[i] = spec && b < n_approx ? ws->list_rec[b][i] : 0.0f;
+    uint32_t v = (uint32_t)(ent[0] >> 32);  // the workgroup's largest key
+    if (tid == 0)
+        s_count = 0;
+    uint32_t low = 0xffffffffu;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const uint32_t m = wave_max_u32(v);
+        low = min(low, m);
+        const uint64_t holders = __ballot(v == m);
+        if (lane == __ffsll((unsigned long long)holders) - 1)
+            v = 0;
+    }
+    const uint32_t nmax = wave_max_u32((uint32_t)(ent[kListLen] >> 32));
+    if (lane == 0) {
+        wave_low[w] = low;
+        wave_next[w] = nmax;
+    }
+    __syncthreads();
+    uint32_t L = wave_low[0], max_next = wave_next[0];
+#pragma unroll
+    for (int i = 1; i < kSelectBlock / 64; ++i) {
+        L = min(L, wave_low[i]);
+        max_next = max(max_next, wave_next[i]);
+    }
+    L = max(L, 1u);  // key 0 marks "no element"
+#pragma unroll
+    for (int i = 0; i < kListLen; ++i) {
+        const uint32_t k = (uint32_t)(ent[i] >> 32);
+        pool_append(k >= L, k, (int32_t)(uint32_t)ent[i], pool, &s_count, kMergeCap, erec[i], pool_rec);
+    }
+    __syncthreads();
+    int n_pool = s_count;
+    bool exact = n_pool <= kMergeCap;
+    if (exact) {
+        rank_pool(pool, n_pool, kk, sel, pool_rec, sel_rec);
+        exact = n_pool >= kk && max_next < sel[kk - 1].key;
+    }
+    if (!exact) {
+        // the lists may miss elements: every logit at or above L
+        __syncthreads();
+        if (tid == 0)
+            s_count = 0;
+        __syncthreads();
         for (int e0 = tid; e0 < V; e0 += kScanUnroll * kSelectBlock) {
             uint32_t g[kScanUnroll];  // all loads of the batch in flight at once
 #pragma unroll
@@ -413,161 +659,57 @@ __global__ __launch_bounds__(kSelectBlock) void k_head_select(const float* __res
             }
 #pragma unroll
             for (int u = 0; u < kScanUnroll; ++u)
-                tmax = max(tmax, g[u]);
-        }
-    }
-    for (int k = tid; k < K; k += kSelectBlock)  // K <= kHeadMaxChunks * 256
-        xs[k] = x[k];
-    uint32_t v = tmax, low = 0xffffffffu;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const uint32_t m = wave_max_u32(v);
-        low = min(low, m);
-        const uint64_t holders = __ballot(v == m);
-        if (lane == __ffsll((unsigned long long)holders) - 1)
-            v = 0;
-    }
-    if (lane == 0)
-        wave_low[w] = low;
-    if (tid == 0)
-        s_pool = 0;
-    __syncthreads();
-    uint32_t L = wave_low[0];
-#pragma unroll
-    for (int i = 1; i < kSelectBlock / 64; ++i)
-        L = min(L, wave_low[i]);
-    L = max(L, 1u);  // key 0 marks "no element"
-    // the pool: every element with key >= L (all of the kk best among them)
-    if (in_regs) {
-#pragma unroll
-        for (int u = 0; u < kRegLogits; ++u) {
-            const int e = tid + u * kSelectBlock;
-            const uint32_t k = e < V ? order_key(f[u]) : 0u;
-            pool_append(k >= L, k, e, pool, &s_pool, kSelectBlock);
-        }
-    } else {
-        for (int e0 = tid; e0 < V; e0 += kScanUnroll * kSelectBlock) {
-            uint32_t g[kScanUnroll];
-#pragma unroll
-            for (int u = 0; u < kScanUnroll; ++u) {
-                const int e = e0 + u * kSelectBlock;
-                g[u] = e < V ? order_key(logits[e]) : 0u;
-            }
-#pragma unroll
-            for (int u = 0; u < kScanUnroll; ++u)
-                pool_append(g[u] >= L, g[u], e0 + u * kSelectBlock, pool, &s_pool, kSelectBlock);
-        }
-    }
-    __syncthreads();
-    const int n_pool = s_pool;
-    if (n_pool <= kSelectBlock) {
-        // the rank of a pooled entry is the number of entries that precede it
-        // (a strict total order), so the kk best land in sel by rank
-        if (tid < n_pool) {
-            const Entry me = pool[tid];
-            int rank = 0;
-            int j = 0;
-            for (; j + 8 <= n_pool; j += 8) {  // eight LDS reads in flight
-                Entry o[8];
-#pragma unroll
-                for (int t = 0; t < 8; ++t)
-                    o[t] = pool[j + t];
-#pragma unroll
-                for (int t = 0; t < 8; ++t)
-                    rank += precedes(o[t], me);
-            }
-            for (; j < n_pool; ++j)
-                rank += precedes(pool[j], me);
-            if (rank < kk)
-                sel[rank] = me;
+                pool_append(g[u] >= L, g[u], e0 + u * kSelectBlock, pool, &s_count, kMergeCap);
         }
         __syncthreads();
-    } else {
-        // too many equal keys at the bound: select over the whole array
-        __syncthreads();
-        radix_select_all(logits, V, kk, sel, hist, scan);
-        if (tid < kHeadMaxK && tid >= kk)
-            sel[tid] = Entry{0u, 0x7fffffff};
-        __syncthreads();
-        bitonic_sort<kHeadMaxK>(sel);
+        n_pool = s_count;
+        if (n_pool <= kMergeCap) {
+            rank_pool(pool, n_pool, kk, sel);
+        } else {
+            radix_select_all(logits, V, kk, sel, hist, scan);
+            if (tid < kHeadMaxK && tid >= kk)
+                sel[tid] = Entry{0u, 0x7fffffff};
+            __syncthreads();
+            bitonic_sort<kHeadMaxK>(sel);
+        }
     }
 
     const float l1 = key_value(sel[0].key);
     const float gap = V >= 2 ? l1 - key_value(sel[1].key) : __builtin_inff();
     const bool verify = gap < threshold;
-    if (tid < top_k) {
+    if (tid < top_k)
         cand[tid] = sel[tid].row;
-        if (!verify)
-            cand_logits[tid] = key_value(sel[tid].key);
-    }
     if (!verify) {
+        if (tid < top_k)
+            cand_logits[tid] = key_value(sel[tid].key);
         if (tid == 0) {
             result[0] = sel[0].row;
             result[1] = 0;
         }
         return;
     }
-
-    // Recompute the candidates with the FP32 activations.  Wave w takes
-    // candidates w + 16 r (r < 4); lane l covers bytes 16 l + 1024 c of a row
-    // (c < ceil(K / 1024)); all four rows' weights are loaded before any is
-    // summed, so the 64 rows cost one memory round trip.
-    constexpr int kRowsPerWave = kHeadMaxK / (kSelectBlock / 64);
-    constexpr int kRowsAtOnce = 4;
-    constexpr int kMaxC = kHeadMaxChunks * 256 / 1024;
-    const int n_c = (K + 1023) / 1024;
-    for (int r0 = 0; r0 < kRowsPerWave; r0 += kRowsAtOnce) {
-    u32x4 qd[kRowsAtOnce][kMaxC];
-    float srow[kRowsAtOnce];  // the rows' scales, loaded with their weights
-#pragma unroll
-    for (int r = 0; r < kRowsAtOnce; ++r) {
-        const int i = w + (kSelectBlock / 64) * (r0 + r);
-        srow[r] = i < top_k ? scale[sel[i].row] : 0.0f;
-        const int8_t* qrow = Q + (int64_t)(i < top_k ? sel[i].row : 0) * K;
-#pragma unroll
-        for (int c = 0; c < kMaxC; ++c) {
-            const int k = 16 * lane + 1024 * c;
-            qd[r][c] = (i < top_k && c < n_c && k < K) ? *reinterpret_cast<const u32x4*>(qrow + k)  // Q 16-byte aligned
-                                                        : u32x4{0, 0, 0, 0};
+    if (!(exact && spec)) {
+        // wave w recomputes candidates w, w + 16, w + 32, w + 48
+        for (int i = w; i < top_k; i += kSelectBlock / 64) {
+            const float r = recompute_row(Q, scale, K, x, sel[i].row);
+            if (lane == 0)
+                sel_rec[i] = r;
         }
+        __syncthreads();
     }
-#pragma unroll
-    for (int r = 0; r < kRowsAtOnce; ++r) {
-        const int i = w + (kSelectBlock / 64) * (r0 + r);
-        float acc = 0.0f;
-#pragma unroll
-        for (int c = 0; c < kMaxC; ++c) {
-            const int k = 16 * lane + 1024 * c;
-            if (c < n_c && k < K) {
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const uint32_t d = qd[r][c][t];
-                    const f32x4 x4 = *reinterpret_cast<const f32x4*>(xs + k + 4 * t);
-                    acc = __builtin_fmaf(cvt_i8<0>(d), x4.x, acc);
-                    acc = __builtin_fmaf(cvt_i8<1>(d), x4.y, acc);
-                    acc = __builtin_fmaf(cvt_i8<2>(d), x4.z, acc);
-                    acc = __builtin_fmaf(cvt_i8<3>(d), x4.w, acc);
-                }
-            }
+    if (tid < top_k)
+        cand_logits[tid] = sel_rec[tid];
+    if (w == 0) {
+        // the largest recomputed logit, ties to the lower row: wave maximum
+        // of the key, then the least row holding it
+        const uint32_t key = lane < top_k ? order_key(sel_rec[lane]) : 0u;
+        const uint32_t top = wave_max_u32(key);
+        const uint32_t row = key == top ? (uint32_t)sel[lane].row : 0xffffffffu;
+        const uint32_t least = ~wave_max_u32(~row);
+        if (lane == 0) {
+            result[0] = (int32_t)least;
+            result[1] = 1;
         }
-#pragma unroll
-        for (int dd = 32; dd >= 1; dd >>= 1)
-            acc += __shfl_xor(acc, dd, 64);
-        if (lane == 0 && i < top_k) {
-            const float res_i = acc * srow[r];
-            rec[i] = res_i;
-            cand_logits[i] = res_i;
-        }
-    }
-    }
-    __syncthreads();
-    if (tid == 0) {
-        int best = 0;
-        for (int i = 1; i < top_k; ++i)
-            if (rec[i] > rec[best] || (rec[i] == rec[best] && sel[i].row < sel[best].row))
-                best = i;
-        result[0] = sel[best].row;
-        result[1] = 1;
     }
 }
 

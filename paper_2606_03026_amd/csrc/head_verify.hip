@@ -1,5 +1,5 @@
 // Host side of the output-head candidate verification (C ABI in
-// include/head_verify.h): validation and the two launches.
+// include/head_verify.h): validation and the launches.
 #include "head_verify.h"
 
 #include <hip/hip_runtime.h>
@@ -16,25 +16,26 @@ namespace {
 using spk::fail;
 using spk::hip_fail;
 
-using ApproxFn = void (*)(const int8_t*, const float*, int, int, const float*, float*);
+using ApproxFn = void (*)(const int8_t*, const float*, int, int, const float*, float*, uint64_t*, float*);
 
-template <int NPL>
+template <int NPL, bool SPEC>
 ApproxFn approx_fn()
 {
-    return spk::k_head_approx<NPL, (NPL >= 4 ? 2 : 8 / NPL)>;
+    return spk::k_head_approx<NPL, (NPL >= 4 ? 2 : 8 / NPL), SPEC>;
 }
 
+template <bool SPEC>
 ApproxFn pick_approx(int npl)
 {
     switch (npl) {
-    case 1: return approx_fn<1>();
-    case 2: return approx_fn<2>();
-    case 3: return approx_fn<3>();
-    case 4: return approx_fn<4>();
-    case 5: return approx_fn<5>();
-    case 6: return approx_fn<6>();
-    case 7: return approx_fn<7>();
-    default: return approx_fn<8>();
+    case 1: return approx_fn<1, SPEC>();
+    case 2: return approx_fn<2, SPEC>();
+    case 3: return approx_fn<3, SPEC>();
+    case 4: return approx_fn<4, SPEC>();
+    case 5: return approx_fn<5, SPEC>();
+    case 6: return approx_fn<6, SPEC>();
+    case 7: return approx_fn<7, SPEC>();
+    default: return approx_fn<8, SPEC>();
     }
 }
 
@@ -44,9 +45,11 @@ bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0;
 
 extern "C" {
 
+int64_t head_verify_workspace_bytes(void) { return (int64_t)sizeof(spk::HeadWorkspace); }
+
 int head_verify_forward(const int8_t* Q, const float* scale, int32_t K, int32_t V, const float* x, int32_t top_k,
                         float threshold, float* logits, int32_t* cand, float* cand_logits, int32_t* result,
-                        void* stream)
+                        void* workspace, void* stream)
 {
     spk::last_error.clear();
     if (K < 16 || K > HEAD_MAX_K || K % 16 != 0)
@@ -57,21 +60,26 @@ int head_verify_forward(const int8_t* Q, const float* scale, int32_t K, int32_t 
         return fail(SPIKE_EINVAL, "top_k = %d outside [1, min(%d, V = %d)]", top_k, HEAD_MAX_TOP_K, V);
     if (std::isnan(threshold))
         return fail(SPIKE_EINVAL, "threshold is NaN");
-    if (!Q || !scale || !x || !logits || !cand || !cand_logits || !result)
+    if (!Q || !scale || !x || !logits || !cand || !cand_logits || !result || !workspace)
         return fail(SPIKE_EINVAL, "null pointer argument");
-    if (!aligned(Q, 16))
-        return fail(SPIKE_EINVAL, "Q must be 16-byte aligned");
+    if (!aligned(Q, 16) || !aligned(workspace, 16))
+        return fail(SPIKE_EINVAL, "Q and the workspace must be 16-byte aligned");
     if (!aligned(scale, 4) || !aligned(x, 4) || !aligned(logits, 4) || !aligned(cand, 4) ||
         !aligned(cand_logits, 4) || !aligned(result, 4))
         return fail(SPIKE_EINVAL, "scale, x and the outputs must be 4-byte aligned");
     const hipStream_t st = static_cast<hipStream_t>(stream);
+    auto* ws = static_cast<spk::HeadWorkspace*>(workspace);
     const int npl = (K + 511) / 512;
     const int64_t groups = ((int64_t)V + 1) / 2 * 2;
     const int64_t wgs = std::max<int64_t>(1, std::min<int64_t>((groups + spk::kRegGroups - 1) / spk::kRegGroups,
-                                                               256 * 2));
-    hipLaunchKernelGGL(pick_approx(npl), dim3((unsigned)wgs), dim3(spk::kRegBlock), 0, st, Q, scale, K, V, x, logits);
-    hipLaunchKernelGGL(spk::k_head_select, dim3(1), dim3(spk::kSelectBlock), 0, st, logits, V, top_k, threshold, Q,
-                       scale, K, x, cand, cand_logits, result);
+                                                               spk::kApproxMaxWgs));
+    // a gap is never negative, so only a threshold > 0 can ask for verification:
+    // then the approximate head also recomputes its listed rows
+    const bool spec = threshold > 0.0f;
+    hipLaunchKernelGGL(spec ? pick_approx<true>(npl) : pick_approx<false>(npl), dim3((unsigned)wgs),
+                       dim3(spk::kRegBlock), 0, st, Q, scale, K, V, x, logits, &ws->lists[0][0], &ws->list_rec[0][0]);
+    hipLaunchKernelGGL(spk::k_head_select, dim3(1), dim3(spk::kSelectBlock), 0, st, logits, V, top_k, threshold,
+                       (int)wgs, (int)spec, ws, Q, scale, K, x, cand, cand_logits, result);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return hip_fail(e, "head verification launch");

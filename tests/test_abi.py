@@ -212,14 +212,19 @@ def test_head_verify_argument_validation_before_any_hip_call(sp):
     lib = sp.raw_library()
     d = 0x1000  # never dereferenced: validation fails first
     f = lib.head_verify_forward
-    assert f(d, d, 24, 100, d, 8, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL  # K % 16
-    assert f(d, d, 4112, 100, d, 8, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL  # K too large
-    assert f(d, d, 1536, 0, d, 8, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL
-    assert f(d, d, 1536, 100, d, 0, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL
-    assert f(d, d, 1536, 100, d, 65, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL
-    assert f(d, d, 1536, 5, d, 6, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL  # top_k > V
-    assert f(d, d, 1536, 100, d, 8, float("nan"), d, d, d, d, None) == sp.SPIKE_EINVAL
+    assert f(d, d, 24, 100, d, 8, 0.5, d, d, d, d, d, None) == sp.SPIKE_EINVAL  # K % 16
+    assert f(d, d, 4112, 100, d, 8, 0.5, d, d, d, d, d, None) == sp.SPIKE_EINVAL  # K too large
+    assert f(d, d, 1536, 0, d, 8, 0.5, d, d, d, d, d, None) == sp.SPIKE_EINVAL
+    assert f(d, d, 1536, 100, d, 0, 0.5, d, d, d, d, d, None) == sp.SPIKE_EINVAL
+    assert f(d, d, 1536, 100, d, 65, 0.5, d, d, d, d, d, None) == sp.SPIKE_EINVAL
+    assert f(d, d, 1536, 5, d, 6, 0.5, d, d, d, d, d, None) == sp.SPIKE_EINVAL  # top_k > V
+    assert f(d, d, 1536, 100, d, 8, float("nan"), d, d, d, d, d, None) == sp.SPIKE_EINVAL
     assert "NaN" in sp.spike_proj_last_error()
-    assert f(d + 4, d, 1536, 100, d, 8, 0.5, d, d, d, d, None) == sp.SPIKE_EINVAL
+    assert f(d + 4, d, 1536, 100, d, 8, 0.5, d, d, d, d, d, None) == sp.SPIKE_EINVAL
     assert "16-byte" in sp.spike_proj_last_error()
-    assert f(d, d, 1536, 100, d, 8, 0.5, None, d, d, d, None) == sp.SPIKE_EINVAL
+    assert f(d, d, 1536, 100, d, 8, 0.5, None, d, d, d, d, None) == sp.SPIKE_EINVAL
+    assert f(d, d, 1536, 100, d, 8, 0.5, d, d, d, d, None, None) == sp.SPIKE_EINVAL  # no workspace
+    assert f(d, d, 1536, 100, d, 8, 0.5, d, d, d, d, d + 8, None) == sp.SPIKE_EINVAL
+    assert "workspace" in sp.spike_proj_last_error()
+    n = lib.head_verify_workspace_bytes()
+    assert 0 < n < 1 << 20 and n % 16 == 0

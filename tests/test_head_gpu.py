@@ -143,6 +143,48 @@ def test_exact_ties_take_lower_rows(sp):
     assert list(got["cand"]) == list(range(64)) and got["verified"] and got["token"] == 0
 
 
+@pytest.mark.parametrize("step", [13, 40])
+def test_ties_across_selecting_workgroups(sp, step):
+    """Rows every `step`-th of 20,000 hold the same largest logit: 1,539 tied
+    rows overflow the pools (radix select over the whole array), 500 tied rows
+    spread over the five selecting workgroups are merged and ranked."""
+    V, K = 20000, 32
+    rng = np.random.default_rng([42, 18, step])
+    Q = rng.integers(-3, 4, size=(V, K)).astype(np.int8)
+    Q[::step] = 100
+    s = np.full(V, 0.003, dtype=np.float32)
+    x = np.abs(rng.standard_normal(K)).astype(np.float32) + 0.5
+    for k, thr in ((64, 0.5), (3, float("inf")), (1, 0.0)):
+        got = gpu_head(sp, Q, s, x, k, thr)
+        ref = assert_head_parity(got, Q, s, x, k, thr)
+        assert list(ref["cand"]) == list(range(0, step * k, step))
+
+
+def test_workspace_shared_by_calls(sp):
+    """One explicit workspace, filled with junk first, through calls of
+    different sizes, gates and selection paths on one stream."""
+    ws = sp.head_verify_workspace()
+    ws.fill_(0xA5)
+    d = wl.dense_projection("head", B=1)
+    x = np.random.default_rng(9).standard_normal(1536).astype(np.float32)
+    Qt, st_, _ = head_problem(20000, 256, 5)
+    cases = [(d["Q"], d["scale"], x, 64, float("inf")), (np.zeros((3000, 32), dtype=np.int8),
+             np.ones(3000, dtype=np.float32), x[:32], 8, 0.5), (Qt, st_, x[:256], 16, 4.0),
+             (d["Q"][:1], d["scale"][:1], x, 1, 0.5), (d["Q"], d["scale"], x, 2, 0.0)]
+    for Q, s, xx, k, thr in cases:
+        V = Q.shape[0]
+        logits = torch.empty(V, device="cuda")
+        cand = torch.empty(k, dtype=torch.int32, device="cuda")
+        cl = torch.empty(k, device="cuda")
+        res = torch.empty(2, dtype=torch.int32, device="cuda")
+        sp.head_verify_forward(dev(Q), dev(s), dev(xx), k, thr, logits, cand, cl, res, workspace=ws)
+        torch.cuda.synchronize()
+        got = dict(logits=logits.cpu().numpy(), cand=cand.cpu().numpy(), cand_logits=cl.cpu().numpy(),
+                   token=int(res[0]), verified=bool(res[1]))
+        assert_head_parity(got, Q, s, xx, k, thr)
+
+
+
 def test_negative_and_mixed_logits(sp):
     Q, s, x = head_problem(5000, 256, 2)
     Q[:2500] = -np.abs(Q[:2500])
