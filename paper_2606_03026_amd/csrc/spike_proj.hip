@@ -798,16 +798,18 @@ int spike_stack_forward_fused(const spike_proj_t* projs, int32_t n_proj, const u
     if (int rc = check_device(projs[0]->device))
         return rc;
     // one ring plan for all items, chosen for the shortest K (every wave needs a k-step)
-    // Tiles of up to 64 rows by 48 channels, 16 waves, two k-steps in flight
-    // per wave (measured best on the 64-row decode stack: 1408 workgroups
-    // over 44 projections); the first handle's matrix-core tuning knobs
-    // override it for the whole launch.
+    // Tiles of up to 64 rows by 48 channels, two k-steps in flight per wave;
+    // 8 waves for 64-row tiles (measured on the 64-row decode stack, 1408
+    // workgroups over 44 projections: 49 us per step against 57 us with 16
+    // waves, 53 with 4), 16 for the narrower tiles of smaller batches; the
+    // first handle's matrix-core tuning knobs override it for the whole
+    // launch.
     const spike_proj* h0 = projs[0];
     const int sets = N / spk::kMfmaNAlign;
     spk::MfmaPlan p{};
     p.rt = B <= 16 ? 1 : B <= 32 ? 2 : 4;
     p.cs = sets % 3 == 0 ? 3 : sets % 2 == 0 ? 2 : 1;
-    p.kw = 16;
+    p.kw = p.rt >= 4 ? 8 : 16;
     p.d = 2;
     if (h0->mfma_row_tile > 0)
         p.rt = h0->mfma_row_tile;
