@@ -209,10 +209,12 @@ int spike_proj_tune(spike_proj_t h, int32_t key, int32_t value);
 int spike_proj_shapes(int32_t *codes, int32_t cap);
 
 /* The matrix-core plans this build instantiates, as codes
- * rt | cs << 4 | kw << 8 | d << 16 | preload << 24 (16-row subtiles and
- * 16-channel sets per workgroup, waves, k-steps of weights in flight per
- * wave, all loads issued at once): writes up to `cap` codes to `codes`
- * (host memory; may be NULL when cap is 0) and returns how many exist. */
+ * rt | cs << 4 | kw << 8 | d << 16 | preload << 24 | direct << 25 (16-row
+ * subtiles and 16-channel sets per workgroup, waves, k-steps of weights in
+ * flight per wave, all loads issued at once, spike words loaded with each
+ * k-step instead of staged in LDS; the automatic plan of batches up to 4
+ * rows is direct): writes up to `cap` codes to `codes` (host memory; may be
+ * NULL when cap is 0) and returns how many exist. */
 int spike_mfma_plans(int32_t *codes, int32_t cap);
 
 /* Which path a forward() of B rows takes on a handle created for a K x N

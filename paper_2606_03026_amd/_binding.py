@@ -308,7 +308,7 @@ def spike_mfma_plans() -> list:
 
 def decode_plan(code: int) -> dict:
     return {"rt": code & 15, "cs": (code >> 4) & 15, "kw": (code >> 8) & 255, "d": (code >> 16) & 255,
-            "preload": bool((code >> 24) & 1)}
+            "preload": bool((code >> 24) & 1), "direct": bool((code >> 25) & 1)}
 
 
 def spike_proj_plan_query(K: int, N: int, B: int):

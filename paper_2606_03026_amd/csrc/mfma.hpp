@@ -25,7 +25,9 @@
 // registers from bits 16q .. 16q + 15 of the row's mask word (one byte of 0
 // or 1 per bit).  The workgroup first stages the mask words of its rows in
 // LDS with coalesced loads (row pitch odd in words, so that the 16 rows of
-// one operand read sit in distinct banks).  Result layout of the 16x16 i32
+// one operand read sit in distinct banks); for batches of at most 4 rows each
+// lane instead loads the dword holding its 16 bits with each k-step's
+// weights (DIRECT plans).  Result layout of the 16x16 i32
 // accumulator (checked on the device): lane l, register j holds row
 // 4*(l/16) + j, column l%16.
 //
@@ -122,16 +124,21 @@ __device__ inline void mfma_tile_of(int id, int n_rowtiles, int n_coltiles, int*
     }
 }
 
-// Bytes of dynamic LDS of one workgroup: the partial-sum tile, then the
-// staged spike words of its rows.
-inline int mfma_lds_bytes(int RT, int CS, int wpr)
+// Bytes of dynamic LDS of one workgroup: the partial-sum tile, then (unless
+// the spike words are loaded directly) the staged spike words of its rows.
+inline int mfma_lds_bytes(int RT, int CS, int wpr, bool direct = false)
 {
-    return RT * CS * 256 * (int)sizeof(int32_t) + 16 * RT * mfma_stage_pitch(wpr) * (int)sizeof(uint64_t);
+    return RT * CS * 256 * (int)sizeof(int32_t) +
+           (direct ? 0 : 16 * RT * mfma_stage_pitch(wpr) * (int)sizeof(uint64_t));
 }
 
 // One output tile (tile id `id` of the launch's n_rowtiles x n_coltiles
-// tiles) of one projection.
-template <int RT, int CS, int KW, int D, bool PRELOAD, bool ACC>
+// tiles) of one projection.  DIRECT: instead of staging the tile's spike
+// words in LDS behind a barrier, each lane loads the dword holding its 16
+// bits of the step with that step's weights (for the smallest batches, where
+// the staging round trip is a large share of a call and the extra loads find
+// rows past B out of range, so they move no data).
+template <int RT, int CS, int KW, int D, bool PRELOAD, bool ACC, bool DIRECT = false>
 // Always inlined: as a called function it spills (the call ABI) and runs
 // several times slower.
 __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __restrict__ P, const float* __restrict__ scale, int N,
@@ -143,7 +150,7 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
     constexpr int RED = RT * CS * 256;  // INT32 entries of the partial-sum tile
     extern __shared__ __align__(16) uint8_t lds[];
     int32_t* red = reinterpret_cast<int32_t*>(lds);
-    uint64_t* xs = reinterpret_cast<uint64_t*>(lds + RED * sizeof(int32_t));
+    uint64_t* xs = reinterpret_cast<uint64_t*>(lds + RED * sizeof(int32_t));  // staged spike words (!DIRECT)
     const int pitch = wpr | 1;
 
     // wave index as a scalar, so that everything derived from it (k-steps,
@@ -164,12 +171,23 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
     // vector register, the k-step a scalar, so addressing costs no vector ALU.
     const __amdgpu_buffer_rsrc_t prsrc = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<int8_t*>(P), 0, (N / 16) * wpr * kMfmaSetStepBytes, kBufferWordFormat);
-    auto load_w = [&](int i, u32x4 (&wv)[CS]) {
+    // The mask is a buffer resource: rows at or past B read as 0.
+    const __amdgpu_buffer_rsrc_t mrsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint64_t*>(mask), 0, B * wpr * (int)sizeof(uint64_t), kBufferWordFormat);
+    // Weights of the wave's step i; DIRECT: also, per row subtile, the dword
+    // holding bits 16q .. 16q + 15 of word s of row 16 ms + c.
+    auto load_w = [&](int i, u32x4 (&wv)[CS], uint32_t (&bv)[RT]) {
         const int s = wave + i * KW;
 #pragma unroll
         for (int t = 0; t < CS; ++t)
             wv[t] = __builtin_amdgcn_raw_buffer_load_b128(prsrc, 16 * l,
                                                           ((t0 + t) * wpr + s) * kMfmaSetStepBytes, 0);
+        if constexpr (DIRECT) {
+#pragma unroll
+            for (int ms = 0; ms < RT; ++ms)
+                bv[ms] = __builtin_amdgcn_raw_buffer_load_b32(
+                    mrsrc, ((m0 + 16 * ms + c) * wpr + s) * (int)sizeof(uint64_t) + 4 * (q / 2), 0, 0);
+        }
     };
 
     // Output form (see the final loops).  Tall tiles (RT >= 4: batches of
@@ -210,15 +228,17 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
     // step: a conditional load would turn its registers into phis that the
     // compiler fills with copies.
     u32x4 wbuf[D][CS];
+    uint32_t bbuf[D][RT];  // DIRECT: the spike dwords of each slot
 #pragma unroll
     for (int d = 0; d < D; ++d)
-        load_w(min(d, n_steps - 1), wbuf[d]);
+        load_w(min(d, n_steps - 1), wbuf[d], bbuf[d]);
 
-    // Stage the tile's spike words (ROWS rows x wpr words), zero the partial
-    // tile.  The mask is a buffer resource, so rows at or past B read as 0.
-    {
-        const __amdgpu_buffer_rsrc_t mrsrc = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<uint64_t*>(mask), 0, B * wpr * (int)sizeof(uint64_t), kBufferWordFormat);
+    // Stage the tile's spike words (ROWS rows x wpr words) unless DIRECT,
+    // and zero the partial tile.
+    if constexpr (DIRECT) {
+        for (int e = threadIdx.x; e < RED; e += BLOCK)
+            red[e] = 0;
+    } else {
         const int total = ROWS * wpr;
         // loads in flight per thread before their stores: enough that a
         // tile of up to 128 words per row is staged in one round trip
@@ -245,8 +265,8 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
         }
         for (int e = threadIdx.x; e < RED; e += BLOCK)
             red[e] = 0;
+        __syncthreads();
     }
-    __syncthreads();
 
     mf_i32x4 acc[RT][CS];
 #pragma unroll
@@ -263,6 +283,12 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
 #pragma unroll
         for (int ms = 0; ms < RT; ++ms)
             b[ms] = xs16[((16 * ms + c) * pitch + s) * 4 + q];
+    };
+    // DIRECT: this lane's 16 bits are the low or high half of its dword
+    auto slot_bits = [&](const uint32_t (&bv)[RT], uint32_t (&b)[RT]) {
+#pragma unroll
+        for (int ms = 0; ms < RT; ++ms)
+            b[ms] = bv[ms] >> (16 * (q & 1));
     };
     auto products = [&](const uint32_t (&b)[RT], const u32x4 (&wv)[CS]) {
         mf_i32x4 a[RT];
@@ -283,9 +309,33 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
         for (int d = 0; d < D; ++d)
             if (d < n_steps) {
                 uint32_t b[RT];
-                read_bits(d, b);
+                if constexpr (DIRECT)
+                    slot_bits(bbuf[d], b);
+                else
+                    read_bits(d, b);
                 products(b, wbuf[d]);
             }
+    } else if constexpr (DIRECT) {
+        // Ring of D slots of weights and spike dwords; a slot is refilled
+        // after its products with the step D ahead (clamped, as below).
+        auto step = [&](int i, u32x4 (&wv)[CS], uint32_t (&bv)[RT], bool refill) {
+            uint32_t b[RT];
+            slot_bits(bv, b);
+            products(b, wv);
+            if (refill)
+                load_w(min(i + D, n_steps - 1), wv, bv);
+        };
+        const int n_full = n_steps / D * D;
+        int i0 = 0;
+        for (; i0 < n_full; i0 += D) {
+#pragma unroll
+            for (int d = 0; d < D; ++d)
+                step(i0 + d, wbuf[d], bbuf[d], true);
+        }
+#pragma unroll
+        for (int d = 0; d < D; ++d)
+            if (i0 + d < n_steps)
+                step(i0 + d, wbuf[d], bbuf[d], false);
     } else {
         // Ring of D slots; the loop is unrolled by D so slot indices stay
         // static.  A slot is refilled after its products (the load then
@@ -296,12 +346,12 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
         // latency hides behind the current step's products.
         uint32_t bits[RT];
         read_bits(0, bits);
-        auto step = [&](int i, u32x4 (&wv)[CS], bool refill) {
+        auto step = [&](int i, u32x4 (&wv)[CS], uint32_t (&bv)[RT], bool refill) {
             uint32_t nb[RT];
             read_bits(min(i + 1, n_steps - 1), nb);
             products(bits, wv);
             if (refill)
-                load_w(min(i + D, n_steps - 1), wv);
+                load_w(min(i + D, n_steps - 1), wv, bv);
 #pragma unroll
             for (int ms = 0; ms < RT; ++ms)
                 bits[ms] = nb[ms];
@@ -311,13 +361,15 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
         for (; i0 < n_full; i0 += D) {
 #pragma unroll
             for (int d = 0; d < D; ++d)
-                step(i0 + d, wbuf[d], true);
+                step(i0 + d, wbuf[d], bbuf[d], true);
         }
 #pragma unroll
         for (int d = 0; d < D; ++d)
             if (i0 + d < n_steps)
-                step(i0 + d, wbuf[d], false);
+                step(i0 + d, wbuf[d], bbuf[d], false);
     }
+    if constexpr (DIRECT)
+        __syncthreads();  // the partial tile is zeroed before any wave adds to it
 
     // Partial tiles of the waves -> LDS (integer atomics: order-free).
     // Entry ((ms * CS + t) * 4 + j) * 64 + lane holds register j of lane
@@ -384,14 +436,14 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
     }
 }
 
-template <int RT, int CS, int KW, int D, bool PRELOAD, bool ACC>
+template <int RT, int CS, int KW, int D, bool PRELOAD, bool ACC, bool DIRECT>
 __global__ __launch_bounds__(64 * KW) void k_mfma(const int8_t* __restrict__ P, const float* __restrict__ scale,
                                                   int N, const uint64_t* __restrict__ mask, int wpr, int B,
                                                   int n_rowtiles, int n_coltiles, float* __restrict__ out,
                                                   int32_t* __restrict__ acc_out)
 {
-    mfma_tile<RT, CS, KW, D, PRELOAD, ACC>(P, scale, N, mask, wpr, B, n_rowtiles, n_coltiles, blockIdx.x, out,
-                                           acc_out);
+    mfma_tile<RT, CS, KW, D, PRELOAD, ACC, DIRECT>(P, scale, N, mask, wpr, B, n_rowtiles, n_coltiles, blockIdx.x,
+                                                   out, acc_out);
 }
 
 // Several projections of B given spike rows each, in one launch: item j
@@ -426,7 +478,13 @@ __global__ __launch_bounds__(64 * KW) void k_mfma_items(const MfmaItems items, i
 struct MfmaPlan {
     int rt, cs, kw, d;
     bool preload;
+    bool direct = false;  // spike words loaded per k-step instead of staged in LDS
 };
+
+// Batches up to this many rows load their spike words directly (measured:
+// a batch-1 stack of 44 dependent calls on cold weights takes 184 us with
+// direct loads against 196 us staged; from 8 rows on, staging wins).
+constexpr int kMfmaDirectMaxB = 4;
 
 // Instantiated plans.  Every plan needs KW <= wpr (each wave has at least
 // one k-step); PRELOAD plans also need every wave's k-step count to be at
@@ -448,12 +506,22 @@ struct MfmaPlan {
     X(1, 2, 2, 4, false) X(1, 1, 4, 4, false) X(1, 2, 4, 4, false) X(4, 1, 1, 2, false) X(4, 3, 1, 2, false)     \
     X(4, 1, 2, 2, false) X(4, 3, 2, 2, false)
 
+// Plans also instantiated with direct spike loads: the automatic plans of
+// batches up to kMfmaDirectMaxB rows (one 16-row subtile and one channel set
+// per workgroup; every k-step preloaded for K <= 2048, a ring of 2 beyond).
+#define SPK_MFMA_DIRECT_PLANS(X) \
+    X(1, 1, 1, 4, true) X(1, 1, 2, 4, true) X(1, 1, 4, 4, true) X(1, 1, 8, 4, true) X(1, 1, 16, 2, false)
+
 inline bool mfma_instantiated(const MfmaPlan& p)
 {
     bool found = false;
 #define SPK_FIND(RT, CS, KW, D, PRE) \
     found = found || (p.rt == RT && p.cs == CS && p.kw == KW && p.d == D && p.preload == PRE);
-    SPK_MFMA_PLANS(SPK_FIND)
+    if (p.direct) {
+        SPK_MFMA_DIRECT_PLANS(SPK_FIND)
+    } else {
+        SPK_MFMA_PLANS(SPK_FIND)
+    }
 #undef SPK_FIND
     return found;
 }
@@ -525,6 +593,14 @@ inline MfmaPlan mfma_plan(int K, int N, int B, int rt_req, int cs_req, int kw_re
         if (mfma_instantiated(r))
             p = r;
     }
+    // the smallest batches load their spike words directly where that
+    // variant of the plan exists
+    if (B <= kMfmaDirectMaxB) {
+        MfmaPlan r = p;
+        r.direct = true;
+        if (mfma_instantiated(r))
+            p = r;
+    }
     return p;
 }
 
@@ -555,13 +631,14 @@ inline bool mfma_ring_plan(MfmaPlan& p, int min_wpr, int N)
     return true;
 }
 
-// Plan code reported by the library: rt | cs << 4 | kw << 8 | d << 16 | preload << 24.
+// Plan code reported by the library: rt | cs << 4 | kw << 8 | d << 16 |
+// preload << 24 | direct << 25.
 inline int mfma_plan_code(const MfmaPlan& p)
 {
-    return p.rt | p.cs << 4 | p.kw << 8 | p.d << 16 | (p.preload ? 1 << 24 : 0);
+    return p.rt | p.cs << 4 | p.kw << 8 | p.d << 16 | (p.preload ? 1 << 24 : 0) | (p.direct ? 1 << 25 : 0);
 }
 
-template <int RT, int CS, int KW, int D, bool PRELOAD>
+template <int RT, int CS, int KW, int D, bool PRELOAD, bool DIRECT>
 hipError_t launch_mfma_t(const int8_t* P, const float* scale, int K, int N, const uint64_t* mask, int B,
                          float* out, int32_t* acc, bool want_acc, hipStream_t st)
 {
@@ -569,15 +646,15 @@ hipError_t launch_mfma_t(const int8_t* P, const float* scale, int K, int N, cons
     const int n_coltiles = N / (16 * CS);
     const int n_rowtiles = (B + 16 * RT - 1) / (16 * RT);
     const int64_t units = (int64_t)n_coltiles * n_rowtiles;
-    const int lds = mfma_lds_bytes(RT, CS, wpr);
+    const int lds = mfma_lds_bytes(RT, CS, wpr, DIRECT);
     if (units > 0x7fffffff)
         return hipErrorInvalidValue;
     if (want_acc)
-        hipLaunchKernelGGL((k_mfma<RT, CS, KW, D, PRELOAD, true>), dim3((unsigned)units), dim3(64 * KW), lds, st,
-                           P, scale, N, mask, wpr, B, n_rowtiles, n_coltiles, out, acc);
+        hipLaunchKernelGGL((k_mfma<RT, CS, KW, D, PRELOAD, true, DIRECT>), dim3((unsigned)units), dim3(64 * KW), lds,
+                           st, P, scale, N, mask, wpr, B, n_rowtiles, n_coltiles, out, acc);
     else
-        hipLaunchKernelGGL((k_mfma<RT, CS, KW, D, PRELOAD, false>), dim3((unsigned)units), dim3(64 * KW), lds, st,
-                           P, scale, N, mask, wpr, B, n_rowtiles, n_coltiles, out, acc);
+        hipLaunchKernelGGL((k_mfma<RT, CS, KW, D, PRELOAD, false, DIRECT>), dim3((unsigned)units), dim3(64 * KW),
+                           lds, st, P, scale, N, mask, wpr, B, n_rowtiles, n_coltiles, out, acc);
     return hipGetLastError();
 }
 
@@ -613,10 +690,16 @@ inline int mfma_plan_codes(int32_t* codes, int cap)
     int n = 0;
 #define SPK_CODE(RT, CS, KW, D, PRE)                                      \
     if (codes && n < cap)                                                  \
-        codes[n] = mfma_plan_code(MfmaPlan{RT, CS, KW, D, PRE});           \
+        codes[n] = mfma_plan_code(MfmaPlan{RT, CS, KW, D, PRE, false});    \
     ++n;
     SPK_MFMA_PLANS(SPK_CODE)
 #undef SPK_CODE
+#define SPK_CODE_DIRECT(RT, CS, KW, D, PRE)                               \
+    if (codes && n < cap)                                                  \
+        codes[n] = mfma_plan_code(MfmaPlan{RT, CS, KW, D, PRE, true});     \
+    ++n;
+    SPK_MFMA_DIRECT_PLANS(SPK_CODE_DIRECT)
+#undef SPK_CODE_DIRECT
     return n;
 }
 
@@ -643,9 +726,17 @@ inline hipError_t launch_mfma(const MfmaPlan& p, const int8_t* P, const float* s
 {
 #define SPK_LAUNCH(RT, CS, KW, D, PRE)                                                              \
     if (p.rt == RT && p.cs == CS && p.kw == KW && p.d == D && p.preload == PRE)                  \
-        return launch_mfma_t<RT, CS, KW, D, PRE>(P, scale, K, N, mask, B, out, acc, want_acc, st);
-    SPK_MFMA_PLANS(SPK_LAUNCH)
+        return launch_mfma_t<RT, CS, KW, D, PRE, false>(P, scale, K, N, mask, B, out, acc, want_acc, st);
+#define SPK_LAUNCH_DIRECT(RT, CS, KW, D, PRE)                                                       \
+    if (p.rt == RT && p.cs == CS && p.kw == KW && p.d == D && p.preload == PRE)                  \
+        return launch_mfma_t<RT, CS, KW, D, PRE, true>(P, scale, K, N, mask, B, out, acc, want_acc, st);
+    if (p.direct) {
+        SPK_MFMA_DIRECT_PLANS(SPK_LAUNCH_DIRECT)
+    } else {
+        SPK_MFMA_PLANS(SPK_LAUNCH)
+    }
 #undef SPK_LAUNCH
+#undef SPK_LAUNCH_DIRECT
     return hipErrorInvalidValue;
 }
 

@@ -616,7 +616,7 @@ def plan_shape(plan, seed):
 def test_every_matrix_core_plan(sp):
     """Every instantiated matrix-core plan (tile height and width, waves,
     weight depth, preloaded or ring) against the oracle, on a shape it runs."""
-    plans = sp.spike_mfma_plans()
+    plans = [p for p in sp.spike_mfma_plans() if not p["direct"]]  # direct plans: next test
     assert len(plans) >= 30
     for i, plan in enumerate(plans):
         K, N, B = plan_shape(plan, i)
@@ -635,6 +635,33 @@ def test_every_matrix_core_plan(sp):
         print(f"plan {plan} K={K} N={N} B={B}", flush=True)
         assert_parity(sp, h, p["W"], p["scale"], masks)
         h.close()
+
+
+def test_direct_spike_loads_for_the_smallest_batches(sp):
+    """Batches of at most 4 rows load their spike words with each k-step
+    instead of staging them: every direct plan (K from one word to past 2048,
+    every preload depth and the ring) against the oracle, with junk bits
+    past K, for 1 to 4 rows and channel counts that are and are not a
+    multiple of 8 channel sets."""
+    direct = {tuple(p.values()) for p in sp.spike_mfma_plans() if p["direct"]}
+    assert len(direct) >= 5
+    seen = set()
+    for K in (40, 150, 300, 1536, 2111, 6144):
+        for N in (48, 1536):
+            for B in (1, 2, 3, 4):
+                path, plan = sp.spike_proj_plan_query(K, N, B)
+                assert path == sp.SPIKE_PATH_MFMA and plan["direct"], (K, N, B, plan)
+                seen.add(tuple(plan.values()))
+                p = wl.small_problem(K, N, B, 0.2, seed=K + N + B)
+                masks = p["masks"].copy()
+                if K % 64:
+                    masks[:, -1] |= np.uint64((~((1 << (K % 64)) - 1)) & 0xFFFFFFFFFFFFFFFF)
+                h, *_ = make(sp, p["W"], p["scale"])
+                assert_parity(sp, h, p["W"], p["scale"], masks)
+                h.close()
+    assert seen == direct, (seen, direct)
+    # from 5 rows on, the staged plans
+    assert not sp.spike_proj_plan_query(1536, 1536, 5)[1]["direct"]
 
 
 def test_matrix_core_extremes(sp):
