@@ -211,7 +211,8 @@ def bench_decode_stack(sp, torch, wl, timer, args):
                           "p99_us": round(float(np.percentile(lat, 99)), 2), "tokens": int(lat.size),
                           "gbs_median": round(float(np.median(tok_bytes / lat / 1e3)), 1),
                           "mode": "44 batch-1 projections in stream order per token (HIP graph replay), "
-                                  "warm weights"}
+                                  "one weight set (260 MB of matrix-core weights, more than the 256 MB "
+                                  "Infinity Cache, so each token reads them from HBM)"}
         log(f"per-token latency: median {res['latency']['median_us']} us, p99 {res['latency']['p99_us']} us")
     for s in (cold, warm):
         s.close()
