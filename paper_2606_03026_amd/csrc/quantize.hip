@@ -1,5 +1,5 @@
 // Host side of the INT8 quantizer/exporter (C ABI in include/quantize.h):
-// validation and the two launches.  No allocation, no synchronisation.
+// validation and the launches.  No allocation, no synchronisation.
 #include "quantize.h"
 
 #include <hip/hip_runtime.h>
@@ -50,6 +50,24 @@ int spike_quantize_int8(const float* W, int32_t M, int32_t K, int32_t layout, in
         return fail(SPIKE_EINVAL, "W and scale must be 4-byte aligned");
     const hipStream_t st = static_cast<hipStream_t>(stream);
     const int rows_per_block = spk::kQuantBlock / 64;
+    const dim3 row_grid((M + rows_per_block - 1) / rows_per_block);
+    if (layout == SPIKE_LAYOUT_ROW_MAJOR && K % 4 == 0 && K <= spk::kQuantRowsMaxK && aligned(W, 16) &&
+        aligned(Q, 4)) {
+        // one pass: each row read once, held in registers
+        const int nv = (K + 255) / 256;
+        if (nv <= 2)
+            hipLaunchKernelGGL(spk::k_quant_rows<2>, row_grid, dim3(spk::kQuantBlock), 0, st, W, M, K, Q, scale);
+        else if (nv <= 4)
+            hipLaunchKernelGGL(spk::k_quant_rows<4>, row_grid, dim3(spk::kQuantBlock), 0, st, W, M, K, Q, scale);
+        else if (nv <= 6)
+            hipLaunchKernelGGL(spk::k_quant_rows<6>, row_grid, dim3(spk::kQuantBlock), 0, st, W, M, K, Q, scale);
+        else if (nv <= 8)
+            hipLaunchKernelGGL(spk::k_quant_rows<8>, row_grid, dim3(spk::kQuantBlock), 0, st, W, M, K, Q, scale);
+        else
+            hipLaunchKernelGGL(spk::k_quant_rows<16>, row_grid, dim3(spk::kQuantBlock), 0, st, W, M, K, Q, scale);
+        const hipError_t e = hipGetLastError();
+        return e == hipSuccess ? SPIKE_OK : hip_fail(e, "quantizer launch");
+    }
     hipLaunchKernelGGL(spk::k_quant_scale, dim3((M + rows_per_block - 1) / rows_per_block), dim3(spk::kQuantBlock), 0,
                        st, W, M, K, scale);
     const int tiles_m = (M + spk::kQuantTile - 1) / spk::kQuantTile;

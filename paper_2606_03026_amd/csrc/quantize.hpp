@@ -11,11 +11,14 @@
 // continuous-input layout) or column-major (W_cm[k][m] = Q[m][k], the
 // spike-gated layout, Sec. 2.2).
 //
-// Two passes, both bound by HBM: k_quant_scale reads each row once (one
-// wave per row, a max-reduction over the wave) and writes s; k_quant_tile
-// reads W again in 64 x 64 tiles, quantizes, and writes Q.  For the
-// column-major layout the tile is transposed through LDS so that both the
-// reads (along k) and the writes (along m) are contiguous.
+// Row-major output with rows of at most 4096 values (K % 4 == 0, aligned):
+// one pass, k_quant_rows -- one wave per row holds the row in registers,
+// reduces its maximum over the wave, writes s and the row of Q.  Otherwise
+// two passes, both bound by HBM: k_quant_scale reads each row once (one wave
+// per row, a max-reduction over the wave) and writes s; k_quant_tile reads W
+// again in 64 x 64 tiles, quantizes, and writes Q.  For the column-major
+// layout the tile is transposed through LDS so that both the reads (along k)
+// and the writes (along m) are contiguous.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -49,6 +52,47 @@ __device__ inline int8_t quantize_one(float w, float s)
 {
     const float r = __builtin_rintf(__fdiv_rn(w, s));
     return (int8_t)fminf(fmaxf(r, -127.0f), 127.0f);
+}
+
+// One wave per row, the row in registers: lane l holds the float4 chunks
+// l + 64 j (j < NV) of its row, so K <= 256 NV.  Needs K % 4 == 0, W 16-byte
+// and Q 4-byte aligned (host-checked).
+constexpr int kQuantRowsMaxK = 4096;
+template <int NV>
+__global__ __launch_bounds__(kQuantBlock) void k_quant_rows(const float* __restrict__ W, int M, int K,
+                                                            int8_t* __restrict__ Q, float* __restrict__ scale)
+{
+    const int lane = threadIdx.x % 64;
+    const int m = blockIdx.x * (kQuantBlock / 64) + threadIdx.x / 64;
+    if (m >= M)
+        return;
+    const int n4 = K / 4;
+    const float4* row = reinterpret_cast<const float4*>(W + (int64_t)m * K);
+    float4 w[NV];
+    float amax = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        const int c = lane + 64 * j;
+        w[j] = c < n4 ? row[c] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+#pragma unroll
+    for (int j = 0; j < NV; ++j)
+        amax = fmaxf(amax, fmaxf(fmaxf(fabsf(w[j].x), fabsf(w[j].y)), fmaxf(fabsf(w[j].z), fabsf(w[j].w))));
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1)
+        amax = fmaxf(amax, __shfl_xor(amax, d, 64));
+    const float s = __fdiv_rn(fmaxf(amax, 1e-8f), 127.0f);
+    if (lane == 0)
+        scale[m] = s;
+    uint32_t* dst = reinterpret_cast<uint32_t*>(Q + (int64_t)m * K);
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        const int c = lane + 64 * j;
+        if (c < n4)
+            dst[c] = (uint32_t)(uint8_t)quantize_one(w[j].x, s) | (uint32_t)(uint8_t)quantize_one(w[j].y, s) << 8 |
+                     (uint32_t)(uint8_t)quantize_one(w[j].z, s) << 16 |
+                     (uint32_t)(uint8_t)quantize_one(w[j].w, s) << 24;
+    }
 }
 
 // One 64 x 64 tile (rows m0.., columns k0..) per workgroup.  Each thread

@@ -64,7 +64,11 @@ def lay(sp, name):
     return sp.SPIKE_LAYOUT_ROW_MAJOR if name == "row" else sp.SPIKE_LAYOUT_COL_MAJOR
 
 
-@pytest.mark.parametrize("M,K", [(1, 1), (5, 7), (64, 64), (65, 63), (100, 257), (128, 4), (3, 1000)])
+# row-major rows of K % 4 == 0 up to 4096 values take the one-pass kernel
+# (every register depth: K = 4 .. 512, 1000, 1540, 2048, 4096); the others
+# and every column-major case take the two-pass kernels
+@pytest.mark.parametrize("M,K", [(1, 1), (5, 7), (64, 64), (65, 63), (100, 257), (128, 4), (3, 1000), (33, 1540),
+                                 (7, 2048), (5, 4096), (9, 4100)])
 @pytest.mark.parametrize("layout", LAYOUTS)
 def test_quantizer_matches_oracle(sp, M, K, layout):
     assert_same(sp, weights(M, K, 0), lay(sp, layout))
