@@ -68,8 +68,10 @@ int spike_quantize_int8(const float* W, int32_t M, int32_t K, int32_t layout, in
         const hipError_t e = hipGetLastError();
         return e == hipSuccess ? SPIKE_OK : hip_fail(e, "quantizer launch");
     }
-    hipLaunchKernelGGL(spk::k_quant_scale, dim3((M + rows_per_block - 1) / rows_per_block), dim3(spk::kQuantBlock), 0,
-                       st, W, M, K, scale);
+    if (K % 4 == 0 && aligned(W, 16))
+        hipLaunchKernelGGL(spk::k_quant_scale<true>, row_grid, dim3(spk::kQuantBlock), 0, st, W, M, K, scale);
+    else
+        hipLaunchKernelGGL(spk::k_quant_scale<false>, row_grid, dim3(spk::kQuantBlock), 0, st, W, M, K, scale);
     const int tiles_m = (M + spk::kQuantTile - 1) / spk::kQuantTile;
     const int tiles_k = (K + spk::kQuantTile - 1) / spk::kQuantTile;
     const dim3 grid((unsigned)((int64_t)tiles_m * tiles_k));

@@ -29,7 +29,10 @@ namespace spk {
 constexpr int kQuantBlock = 256;
 constexpr int kQuantTile = 64;  // rows (m) and columns (k) of a tile
 
-// one wave per row: s[m] from the row's largest magnitude
+// one wave per row: s[m] from the row's largest magnitude.  VEC (K % 4 == 0,
+// W 16-byte aligned): 16-byte loads; either way 8 loads per lane are in
+// flight before any is used.
+template <bool VEC>
 __global__ __launch_bounds__(kQuantBlock) void k_quant_scale(const float* __restrict__ W, int M, int K,
                                                              float* __restrict__ scale)
 {
@@ -38,9 +41,35 @@ __global__ __launch_bounds__(kQuantBlock) void k_quant_scale(const float* __rest
     if (m >= M)
         return;
     const float* row = W + (int64_t)m * K;
+    constexpr int kBatch = 8;
     float amax = 0.0f;
-    for (int k = lane; k < K; k += 64)
-        amax = fmaxf(amax, fabsf(row[k]));
+    if constexpr (VEC) {
+        const float4* row4 = reinterpret_cast<const float4*>(row);
+        const int n4 = K / 4;
+        for (int c0 = lane; c0 < n4; c0 += 64 * kBatch) {
+            float4 v[kBatch];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int c = c0 + 64 * u;
+                v[u] = c < n4 ? row4[c] : float4{0.0f, 0.0f, 0.0f, 0.0f};
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u)
+                amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v[u].x), fabsf(v[u].y)), fmaxf(fabsf(v[u].z), fabsf(v[u].w))));
+        }
+    } else {
+        for (int k0 = lane; k0 < K; k0 += 64 * kBatch) {
+            float v[kBatch];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int k = k0 + 64 * u;
+                v[u] = k < K ? row[k] : 0.0f;
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u)
+                amax = fmaxf(amax, fabsf(v[u]));
+        }
+    }
 #pragma unroll
     for (int d = 32; d >= 1; d >>= 1)
         amax = fmaxf(amax, __shfl_xor(amax, d, 64));
