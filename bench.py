@@ -560,9 +560,9 @@ def main(argv=None) -> int:
         return write_traffic_record(*args.traffic_record, args.steps, args.warmup, args.tokens)
 
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the projection shards without communication per output-channel range, but no "
-              "multi-GPU path is built)", file=sys.stderr)
+              "multi-GPU path is implemented)", file=sys.stderr)
         return 2
 
     import torch
