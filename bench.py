@@ -619,7 +619,7 @@ def main(argv=None) -> int:
     cpu = None
     if not args.no_cpu:
         affinity = len(os.sched_getaffinity(0))
-        threads = min(affinity, 16)  # the host share of one GPU on the box
+        threads = min(affinity, 16)  # at most the 16 host cores that serve one GPU
         host, masks, Ks = main_res["host"], main_res["masks"], main_res["Ks"]
         nt = args.cpu_tokens
         v1, t1 = cpu_baseline(host, masks, Ks, nt, 1)
