@@ -23,8 +23,9 @@
 // k_head_select: one workgroup of 1024 threads.  The KK = max(K, 2) largest
 // logits are found on order-preserving 32-bit keys: a lower bound L on the
 // KK-th largest comes from the workgroup maxima, the listed entries at or
-// above L (typically about a hundred) are pooled in LDS and each is placed by
-// its rank among them (equal logits by ascending row).  The lists suffice
+// above L (about a hundred for KK = 64, a few dozen for KK = 16) are pooled
+// in LDS and each is placed by its rank among them (equal logits by
+// ascending row).  The lists suffice
 // when every key they leave out is below the KK-th selected key; otherwise
 // the whole array is scanned (pooling, or past 1024 entries a radix select
 // with digits of 11, 11 and 10 bits).  It then computes the gap
@@ -74,13 +75,23 @@ __device__ inline int8_t quant_act(float v, float s)
     return (int8_t)fminf(fmaxf(__builtin_rintf(__fdiv_rn(v, s)), -127.0f), 127.0f);
 }
 
-// s_x of the activation vector, computed by the whole workgroup.
-template <int BLOCK>
-__device__ inline float activation_scale(const float* __restrict__ x, int K, float* red)
+// s_x of the activation vector and its quantized copy in LDS, computed by the
+// whole workgroup: thread t holds elements t + BLOCK i (i < PER, K <= BLOCK
+// PER), all loaded at once (zeros past K), so the quantization needs no
+// second read of x.
+template <int BLOCK, int PER>
+__device__ inline float quantize_activations(const float* __restrict__ x, int K, float* red, int8_t* xq_lds)
 {
+    const __amdgpu_buffer_rsrc_t xres =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(x), 0, K * 4, kBufferFlags);
+    float xv[PER];
     float amax = 0.0f;
-    for (int k = threadIdx.x; k < K; k += BLOCK)
-        amax = fmaxf(amax, fabsf(x[k]));
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        xv[i] = __builtin_bit_cast(float,
+                                   __builtin_amdgcn_raw_buffer_load_b32(xres, (threadIdx.x + BLOCK * i) * 4, 0, 0));
+        amax = fmaxf(amax, fabsf(xv[i]));
+    }
 #pragma unroll
     for (int d = 32; d >= 1; d >>= 1)
         amax = fmaxf(amax, __shfl_xor(amax, d, 64));
@@ -91,7 +102,13 @@ __device__ inline float activation_scale(const float* __restrict__ x, int K, flo
 #pragma unroll
     for (int w = 1; w < BLOCK / 64; ++w)
         m = fmaxf(m, red[w]);
-    return __fdiv_rn(fmaxf(m, 1e-8f), 127.0f);
+    const float sx = __fdiv_rn(fmaxf(m, 1e-8f), 127.0f);
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+        if (threadIdx.x + BLOCK * i < K)
+            xq_lds[threadIdx.x + BLOCK * i] = quant_act(xv[i], sx);
+    __syncthreads();
+    return sx;
 }
 
 // Order-preserving key of a float: larger floats give larger keys.
@@ -171,11 +188,31 @@ __device__ inline float recompute_row(const int8_t* __restrict__ Q, const float*
     return acc * s;
 }
 
+// Device workspace of one head verification: written by the approximate
+// head, read by the selection of the same call (no state across calls).
+// Workgroup b of the approximate head owns slot (b % 16) 64 + b / 16 of each
+// array, the slot that thread b / 16 of wave b % 16 of the selecting
+// workgroup reads, so that the lists spread evenly over its 16 waves and
+// each wave's loads are contiguous.
+constexpr int kApproxMaxWgs = 512;   // the approximate head's grid is at most this
+constexpr int kListSlots = 1024;     // one per selecting thread
+__device__ inline int list_slot(int b)
+{
+    return (b % 16) * 64 + b / 16;
+}
+struct HeadWorkspace {
+    // per approximate-head workgroup: its kListLen largest logits (key << 32 |
+    // row, largest first, key 0: none), then the largest key it does not list
+    uint64_t lists[kListLen + 1][kListSlots];
+    // the listed rows recomputed with the FP32 activations (when the gate can
+    // ask for verification)
+    float list_rec[kListLen][kListSlots];
+};
+
 template <int NPL, int U, bool SPEC>
 __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restrict__ Q, const float* __restrict__ scale,
                                                            int K, int V, const float* __restrict__ x,
-                                                           float* __restrict__ logits, uint64_t* __restrict__ lists,
-                                                           float* __restrict__ list_rec)
+                                                           float* __restrict__ logits, HeadWorkspace* __restrict__ ws)
 {
     __shared__ float red[kRegBlock / 64];
     __shared__ uint64_t wave_best[kRegBlock / 64][kListLen];
@@ -210,12 +247,9 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
         for (int j = 0; j < NPL; ++j)
             slot[u][j] = __builtin_amdgcn_raw_buffer_load_b128(qres, base + chunk_off[j], 0, 2);
     }
-    const float sx = activation_scale<kRegBlock>(x, K, red);
-    // the vector quantized once per workgroup (each element by one thread),
-    // then this lane's activations as packed INT8 (zeros past K)
-    for (int k = threadIdx.x; k < K; k += kRegBlock)
-        xq_lds[k] = quant_act(x[k], sx);
-    __syncthreads();
+    // the vector quantized once per workgroup (K <= 512 NPL), then this
+    // lane's activations as packed INT8 (zeros past K)
+    const float sx = quantize_activations<kRegBlock, 512 * NPL / kRegBlock>(x, K, red, xq_lds);
     uint32_t xq[NPL][4];
 #pragma unroll
     for (int j = 0; j < NPL; ++j) {
@@ -315,7 +349,7 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
         wave_next[wv] = next;
     }
     __syncthreads();
-    uint64_t* my_list = lists + (int64_t)blockIdx.x * (kListLen + 1);
+    const int my_slot = list_slot(blockIdx.x);
     if (wv == 0) {
         const uint64_t e = lane64 < (kRegBlock / 64) * kListLen ? wave_best[lane64 / kListLen][lane64 % kListLen] : 0ull;
         uint32_t ek = (uint32_t)(e >> 32);
@@ -327,7 +361,7 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
             if (r < kListLen) {
                 const uint32_t row = __builtin_amdgcn_readlane((uint32_t)e, h);
                 if (lane64 == 0) {
-                    my_list[r] = (uint64_t)m << 32 | row;
+                    ws->lists[r][my_slot] = (uint64_t)m << 32 | row;
                     final_row[r] = (int)row;
                     final_key[r] = m;
                 }
@@ -338,14 +372,14 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
                 ek = 0;
         }
         if (lane64 == 0)
-            my_list[kListLen] = (uint64_t)nx << 32;
+            ws->lists[kListLen][my_slot] = (uint64_t)nx << 32;
     }
     if constexpr (SPEC) {
         __syncthreads();
         if (final_key[wv] != 0) {
             const float r = recompute_row(Q, scale, K, x, final_row[wv]);
             if (lane64 == 0)
-                list_rec[(int64_t)blockIdx.x * kListLen + wv] = r;
+                ws->list_rec[wv][my_slot] = r;
         }
     }
 }
@@ -517,46 +551,44 @@ __device__ inline void pool_append(bool take, uint32_t key, int row, Entry* pool
     }
 }
 
-// Device workspace of one head verification: written by the approximate
-// head, read by the selection of the same call (no state across calls).
-constexpr int kApproxMaxWgs = 512;   // the approximate head's grid is at most this
 constexpr int kScanUnroll = 16;      // logits per thread loaded before any is used (full scan)
 constexpr int kMergeCap = 1024;      // pooled entries the selection ranks in LDS
-struct HeadWorkspace {
-    // per approximate-head workgroup: its kListLen largest logits (key << 32 |
-    // row, largest first, key 0: none), then the largest key it does not list
-    uint64_t lists[kApproxMaxWgs][kListLen + 1];
-    // the listed rows recomputed with the FP32 activations (when the gate can
-    // ask for verification)
-    float list_rec[kApproxMaxWgs][kListLen];
-};
 
 // Rank selection of the kk best of n pooled entries into sel: the rank of
 // an entry is the number of entries that precede it (a strict total order).
+// G threads count for each entry (G the largest power of two up to 64 with
+// G n <= the block), thread p of the group over entries p, p + G, ..., and
+// the G partial counts are summed across the group's lanes.
 __device__ inline void rank_pool(const Entry* pool, int n, int kk, Entry* sel, const float* vals = nullptr,
                                  float* sel_vals = nullptr)
 {
     const int tid = threadIdx.x;
-    if (tid < n) {
-        const Entry me = pool[tid];
-        int rank = 0;
-        int j = 0;
-        for (; j + 8 <= n; j += 8) {  // eight LDS reads in flight
+    int G = 1;
+    while (G < 64 && 2 * G * n <= kSelectBlock)
+        G *= 2;
+    const int e = tid / G, p = tid % G;
+    Entry me{0u, 0};
+    int rank = 0;
+    if (e < n) {
+        me = pool[e];
+        // eight LDS reads in flight; past n the last entry is read again and
+        // not counted
+        for (int j = p; j < n; j += 8 * G) {
             Entry o[8];
 #pragma unroll
             for (int t = 0; t < 8; ++t)
-                o[t] = pool[j + t];
+                o[t] = pool[min(j + t * G, n - 1)];
 #pragma unroll
             for (int t = 0; t < 8; ++t)
-                rank += precedes(o[t], me);
+                rank += j + t * G < n && precedes(o[t], me);
         }
-        for (; j < n; ++j)
-            rank += precedes(pool[j], me);
-        if (rank < kk) {
-            sel[rank] = me;
-            if (vals)
-                sel_vals[rank] = vals[tid];
-        }
+    }
+    for (int d = 1; d < G; d <<= 1)  // G is the same in every thread
+        rank += __shfl_xor(rank, d, 64);
+    if (e < n && p == 0 && rank < kk) {
+        sel[rank] = me;
+        if (vals)
+            sel_vals[rank] = vals[e];
     }
     __syncthreads();
 }
@@ -565,9 +597,10 @@ __device__ inline void rank_pool(const Entry* pool, int n, int kk, Entry* sel, c
 // approximate head left, per workgroup, its four largest logits, the largest
 // key it did not list, and (SPEC) the listed rows recomputed with the FP32
 // activations.  A lower bound L on the kk-th largest key: every wave takes
-// the 4 largest workgroup maxima it holds (distinct elements) and L is the
-// least of those 64, so at least 64 >= kk elements have keys >= L.  The
-// listed entries at or above L are pooled and ranked; the result is exact
+// the r = ceil(kk / 16) largest workgroup maxima it holds (distinct
+// elements) and L is the least of those 16 r, so at least kk elements have
+// keys >= L.  The listed entries at or above L are pooled and ranked; the
+// result is exact
 // when every key left out of the lists is below the kk-th selected key.
 // Otherwise (many equal or clustered logits) the whole array is scanned:
 // elements at or above L are pooled and ranked, or, past 1024 of them, a
@@ -603,16 +636,19 @@ __global__ __launch_bounds__(kSelectBlock) void k_head_select(const float* __res
     float erec[kListLen];
 #pragma unroll
     for (int i = 0; i <= kListLen; ++i)
-        ent[i] = b < n_approx ? ws->lists[b][i] : 0ull;
+        ent[i] = b < n_approx ? ws->lists[i][tid] : 0ull;
 #pragma unroll
     for (int i = 0; i < kListLen; ++i)
-        erec[i] = spec && b < n_approx ? ws->list_rec[b][i] : 0.0f;
+        erec[i] = spec && b < n_approx ? ws->list_rec[i][tid] : 0.0f;
     uint32_t v = (uint32_t)(ent[0] >> 32);  // the workgroup's largest key
     if (tid == 0)
         s_count = 0;
     uint32_t low = 0xffffffffu;
+    const int rounds = (kk + kSelectBlock / 64 - 1) / (kSelectBlock / 64);  // 16 rounds >= kk
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
+        if (r >= rounds)
+            break;
         const uint32_t m = wave_max_u32(v);
         low = min(low, m);
         const uint64_t holders = __ballot(v == m);
@@ -632,10 +668,36 @@ __global__ __launch_bounds__(kSelectBlock) void k_head_select(const float* __res
         max_next = max(max_next, wave_next[i]);
     }
     L = max(L, 1u);  // key 0 marks "no element"
+    {
+        // the listed entries at or above L, one LDS atomic per wave: the
+        // lane's count in three ballots, its offset the count of the lanes
+        // below it
+        int cnt = 0;
 #pragma unroll
-    for (int i = 0; i < kListLen; ++i) {
-        const uint32_t k = (uint32_t)(ent[i] >> 32);
-        pool_append(k >= L, k, (int32_t)(uint32_t)ent[i], pool, &s_count, kMergeCap, erec[i], pool_rec);
+        for (int i = 0; i < kListLen; ++i)
+            cnt += (uint32_t)(ent[i] >> 32) >= L;
+        const uint64_t b0 = __ballot(cnt & 1), b1 = __ballot(cnt & 2), b2 = __ballot(cnt & 4);
+        const int total = __popcll(b0) + 2 * __popcll(b1) + 4 * __popcll(b2);
+        if (total > 0) {
+            auto below = [&](uint64_t m) {
+                return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+            };
+            int base = 0;
+            if (lane == 0)
+                base = atomicAdd(&s_count, total);
+            int pos = __builtin_amdgcn_readlane(base, 0) + below(b0) + 2 * below(b1) + 4 * below(b2);
+#pragma unroll
+            for (int i = 0; i < kListLen; ++i) {
+                const uint32_t k = (uint32_t)(ent[i] >> 32);
+                if (k >= L) {
+                    if (pos < kMergeCap) {
+                        pool[pos] = Entry{k, (int32_t)(uint32_t)ent[i]};
+                        pool_rec[pos] = erec[i];
+                    }
+                    ++pos;
+                }
+            }
+        }
     }
     __syncthreads();
     int n_pool = s_count;

@@ -16,7 +16,7 @@ namespace {
 using spk::fail;
 using spk::hip_fail;
 
-using ApproxFn = void (*)(const int8_t*, const float*, int, int, const float*, float*, uint64_t*, float*);
+using ApproxFn = void (*)(const int8_t*, const float*, int, int, const float*, float*, spk::HeadWorkspace*);
 
 template <int NPL, bool SPEC>
 ApproxFn approx_fn()
@@ -77,7 +77,7 @@ int head_verify_forward(const int8_t* Q, const float* scale, int32_t K, int32_t 
     // then the approximate head also recomputes its listed rows
     const bool spec = threshold > 0.0f;
     hipLaunchKernelGGL(spec ? pick_approx<true>(npl) : pick_approx<false>(npl), dim3((unsigned)wgs),
-                       dim3(spk::kRegBlock), 0, st, Q, scale, K, V, x, logits, &ws->lists[0][0], &ws->list_rec[0][0]);
+                       dim3(spk::kRegBlock), 0, st, Q, scale, K, V, x, logits, ws);
     hipLaunchKernelGGL(spk::k_head_select, dim3(1), dim3(spk::kSelectBlock), 0, st, logits, V, top_k, threshold,
                        (int)wgs, (int)spec, ws, Q, scale, K, x, cand, cand_logits, result);
     hipError_t e = hipGetLastError();
