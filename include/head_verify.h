@@ -14,12 +14,13 @@
  *     first, equal logits in ascending row order;
  *  4. gate: gap = fl32(l(1) - l(2)) over the two largest approximate logits of
  *     all V rows (+inf when V = 1); verification runs when gap < threshold;
- *  5. verification: each candidate's logit recomputed with the FP32
- *     activations, scale[m] * sum_k float(Q[m][k]) x_k (FP32 FMAs in a fixed
- *     order: per lane a chain of at most 16 ceil(K/1024) products, a 6-level
- *     lane tree, one multiply; error bound as for dense_proj.h with
- *     h = 16 ceil(K/1024) + 7); the token
- *     is the candidate with the largest recomputed logit (ties: lower row).
+ *  5. verification: each candidate's logit with the FP32 activations,
+ *     scale[m] * sum_k float(Q[m][k]) x_k, in the order of the dense register
+ *     kernel (dense_proj.h), so it is bit for bit dense_proj_forward's output
+ *     for row m: per lane an FMA chain over the 16-byte chunks l + 32 j
+ *     (at most 16 ceil(K/512) products), a 5-level lane tree, one multiply;
+ *     error bound as for dense_proj.h with h = 16 ceil(K/512) + 6.  The
+ *     token is the candidate with the largest such logit (ties: lower row).
  *     Without verification the token is the top candidate.
  *
  * Steps 1-3 and the gate decision are exact (bit-identical to the
@@ -44,9 +45,9 @@
  *                share a workspace must not overlap: enqueue them on one
  *                stream, or give each stream its own workspace.
  * Two kernels are enqueued on `stream` (a hipStream_t, NULL for the default
- * stream): the approximate head, which also recomputes a few likely
- * candidates ahead of the gate when threshold > 0, and the selection, gate
- * and verification.  The gate is decided on the device, so the call never
+ * stream): the approximate head, which when threshold > 0 also computes
+ * every row's FP32-activation logit from the same weight registers and keeps
+ * those of its listed rows, and the selection, gate and verification.  The gate is decided on the device, so the call never
  * waits for the GPU and can be captured in a HIP graph.  Nothing is
  * allocated.
  *

@@ -16,9 +16,11 @@
 // results parked in lanes and stored 32 rows at a time.
 //
 // At the end of k_head_approx each workgroup lists its four largest logits
-// and the largest key it leaves out; when the gate can ask for verification
-// (threshold > 0), its four waves also recompute the four listed rows with
-// the FP32 activations right away, while the approximate head still runs.
+// and the largest key it leaves out.  When the gate can ask for verification
+// (threshold > 0), every row's FP32-activation logit is computed in the same
+// pass from the same weight registers, in the dense register kernel's order
+// (bit for bit that kernel's output for the row), and the listed rows carry
+// theirs: the candidates need no second read of their weights.
 //
 // k_head_select: one workgroup of 1024 threads.  The KK = max(K, 2) largest
 // logits are found on order-preserving 32-bit keys: a lower bound L on the
@@ -30,15 +32,15 @@
 // the whole array is scanned (pooling, or past 1024 entries a radix select
 // with digits of 11, 11 and 10 bits).  It then computes the gap
 // fl32(l(1) - l(2)) and, when it is below the threshold, takes the K
-// candidates' recomputed logits (per lane an FMA chain over its 16-byte
-// chunks, a 6-level lane tree, one multiply by s_m) from the lists, or
-// computes them itself after a whole-array selection, and picks the largest
-// (ties: the lower row).
+// candidates' FP32-activation logits (per lane an FMA chain over its 16-byte
+// chunks l + 32 j, the 32-lane tree, one multiply by s_m) from the lists, or
+// computes them itself in the same order after a whole-array selection, and
+// picks the largest (ties: the lower row).
 //
 // Reading the 57,344 logits, or the 64 candidate rows, from memory in one
 // workgroup is bound by the misses one compute unit keeps in flight; the
-// lists cut the first to 20 KB and the speculative recompute spreads the
-// second over the approximate head's workgroups.
+// lists cut the first to 28 KB and the fused FP32 logits remove the second
+// whenever the lists suffice.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -143,49 +145,52 @@ __device__ inline uint32_t wave_max_u32(uint32_t v)
     return max(max(r0, r1), max(r2, r3));
 }
 
-// FP32 logit of one row with the FP32 activations, computed by one wave:
-// lane l covers bytes 16 l + 1024 c of the row (c < ceil(K / 1024)), all
-// loaded at once; a per-lane FMA chain over its chunks, a 6-level lane tree
-// and one multiply by the row's scale.  Every lane returns the result.
+// FP32 logit of one row with the FP32 activations, computed by one wave in
+// the dense register kernel's order, so the result is bit for bit that
+// kernel's output for the row: lane l of each half-wave covers the 16-byte
+// chunks l + 32 j of the row (j < ceil(K / 512)), one FMA chain over its
+// chunks (j, then byte order), the 32-lane tree, one multiply by the row's
+// scale.  Chunks are loaded four at a time (one batch up to K = 2048).
+// Both half-waves compute it; every lane returns the result.
 __device__ inline float recompute_row(const int8_t* __restrict__ Q, const float* __restrict__ scale, int K,
                                       const float* __restrict__ x, int row)
 {
-    constexpr int kMaxC = kHeadMaxChunks * 256 / 1024;
-    const int lane = threadIdx.x % 64;
-    const int n_c = (K + 1023) / 1024;
+    constexpr int kBatch = 4;
+    const int l = threadIdx.x % kRegLanes;
+    const int n_chunks = K / 16;
+    const int n_j = (n_chunks + kRegLanes - 1) / kRegLanes;
     const int8_t* qrow = Q + (int64_t)row * K;
-    u32x4 qd[kMaxC];
-    f32x4 xv[kMaxC][4];
-#pragma unroll
-    for (int c = 0; c < kMaxC; ++c) {
-        const int k = 16 * lane + 1024 * c;
-        const bool ok = c < n_c && k < K;
-        qd[c] = ok ? *reinterpret_cast<const u32x4*>(qrow + k) : u32x4{0, 0, 0, 0};  // Q 16-byte aligned
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-            xv[c][t] = ok ? f32x4{x[k + 4 * t], x[k + 4 * t + 1], x[k + 4 * t + 2], x[k + 4 * t + 3]}
-                          : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    }
     const float s = scale[row];
     float acc = 0.0f;
+    for (int j0 = 0; j0 < n_j; j0 += kBatch) {
+        u32x4 qd[kBatch];
+        f32x4 xv[kBatch][4];
 #pragma unroll
-    for (int c = 0; c < kMaxC; ++c) {
-        const int k = 16 * lane + 1024 * c;
-        if (c < n_c && k < K) {
+        for (int b = 0; b < kBatch; ++b) {
+            const int c = l + kRegLanes * (j0 + b);
+            const bool ok = j0 + b < n_j && c < n_chunks;
+            qd[b] = ok ? *reinterpret_cast<const u32x4*>(qrow + 16 * c) : u32x4{0, 0, 0, 0};  // Q 16-byte aligned
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const uint32_t d = qd[c][t];
-                acc = __builtin_fmaf(cvt_i8<0>(d), xv[c][t].x, acc);
-                acc = __builtin_fmaf(cvt_i8<1>(d), xv[c][t].y, acc);
-                acc = __builtin_fmaf(cvt_i8<2>(d), xv[c][t].z, acc);
-                acc = __builtin_fmaf(cvt_i8<3>(d), xv[c][t].w, acc);
+            for (int t = 0; t < 4; ++t)
+                xv[b][t] = ok ? f32x4{x[16 * c + 4 * t], x[16 * c + 4 * t + 1], x[16 * c + 4 * t + 2],
+                                      x[16 * c + 4 * t + 3]}
+                              : f32x4{0.0f, 0.0f, 0.0f, 0.0f};  // x is 4-byte aligned
+        }
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b) {
+            if (j0 + b < n_j && l + kRegLanes * (j0 + b) < n_chunks) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const uint32_t d = qd[b][t];
+                    acc = __builtin_fmaf(cvt_i8<0>(d), xv[b][t].x, acc);
+                    acc = __builtin_fmaf(cvt_i8<1>(d), xv[b][t].y, acc);
+                    acc = __builtin_fmaf(cvt_i8<2>(d), xv[b][t].z, acc);
+                    acc = __builtin_fmaf(cvt_i8<3>(d), xv[b][t].w, acc);
+                }
             }
         }
     }
-#pragma unroll
-    for (int dd = 32; dd >= 1; dd >>= 1)
-        acc += __shfl_xor(acc, dd, 64);
-    return acc * s;
+    return group32_sum(acc) * s;
 }
 
 // Device workspace of one head verification: written by the approximate
@@ -247,6 +252,21 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
         for (int j = 0; j < NPL; ++j)
             slot[u][j] = __builtin_amdgcn_raw_buffer_load_b128(qres, base + chunk_off[j], 0, 2);
     }
+    // SPEC: this lane's FP32 activations x[16 c + t] for its chunks c (zeros
+    // past K), as the dense register kernel holds them
+    float xr[SPEC ? NPL : 1][16];
+    if constexpr (SPEC) {
+        const __amdgpu_buffer_rsrc_t xres =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(x), 0, K * 4, kBufferFlags);
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) {
+            const int c = l + kRegLanes * j;
+            const uint32_t base = c < n_chunks ? (uint32_t)(c * 16) * 4u : kOutOfRange;
+#pragma unroll
+            for (int t = 0; t < 16; ++t)
+                xr[j][t] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, base + 4 * t, 0, 0));
+        }
+    }
     // the vector quantized once per workgroup (K <= 512 NPL), then this
     // lane's activations as packed INT8 (zeros past K)
     const float sx = quantize_activations<kRegBlock, 512 * NPL / kRegBlock>(x, K, red, xq_lds);
@@ -266,9 +286,12 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
     };
     float sc = scale_of_step(l);
     int parked = 0;
-    // this lane's five largest stored logits, largest first (key 0: none)
+    float parked32 = 0.0f;  // SPEC: the row's FP32-activation sum
+    // this lane's five largest stored logits, largest first (key 0: none),
+    // with (SPEC) their rows' FP32-activation logits
     uint32_t tk[kListLen + 1] = {};
     int trow[kListLen + 1] = {};
+    float tval[kListLen + 1] = {};
     for (int r0 = 0; r0 < n_steps; r0 += U) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -279,6 +302,20 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
                     acc = __builtin_amdgcn_sdot4((int)slot[u][j][i], (int)xq[j][i], acc, false);
+            float acc32 = 0.0f;
+            if constexpr (SPEC) {
+                // the dense register kernel's chain: chunks j, then byte order
+#pragma unroll
+                for (int j = 0; j < NPL; ++j)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const uint32_t d = slot[u][j][i];
+                        acc32 = __builtin_fmaf(cvt_i8<0>(d), xr[j][4 * i + 0], acc32);
+                        acc32 = __builtin_fmaf(cvt_i8<1>(d), xr[j][4 * i + 1], acc32);
+                        acc32 = __builtin_fmaf(cvt_i8<2>(d), xr[j][4 * i + 2], acc32);
+                        acc32 = __builtin_fmaf(cvt_i8<3>(d), xr[j][4 * i + 3], acc32);
+                    }
+            }
             {
                 const uint32_t base = row_base(r + U);
 #pragma unroll
@@ -289,6 +326,11 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
             const int tot = group32_sum_int(acc);
             if (l == (r & 31))
                 parked = tot;
+            if constexpr (SPEC) {
+                const float tot32 = group32_sum(acc32);
+                if (l == (r & 31))
+                    parked32 = tot32;
+            }
             if (r < n_steps && ((r & 31) == 31 || r == n_steps - 1)) {
                 const int rr = (r & ~31) + l;
                 const int m = q + Gq * rr;
@@ -298,15 +340,19 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
                     logits[m] = lg;
                     uint32_t ck = order_key(lg);
                     int cr = m;
+                    float cv = SPEC ? parked32 * sc : 0.0f;  // the dense kernel's y for row m
 #pragma unroll
                     for (int i = 0; i <= kListLen; ++i) {  // insertion, larger keys first
                         const bool up = ck > tk[i];
                         const uint32_t ok = tk[i];
                         const int orow = trow[i];
+                        const float oval = tval[i];
                         tk[i] = up ? ck : ok;
                         trow[i] = up ? cr : orow;
+                        tval[i] = up ? cv : oval;
                         ck = up ? ok : ck;
                         cr = up ? orow : cr;
+                        cv = up ? oval : cv;
                     }
                 }
                 sc = scale_of_step((r & ~31) + 32 + l);
@@ -316,42 +362,48 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
     // The workgroup's four largest logits and the largest key it leaves out:
     // each wave pops its lanes' heads five times, then wave 0 merges the
     // waves' entries the same way.  The selection takes the candidates from
-    // these lists.  With SPEC (a gate that can ask for verification), wave w
-    // also recomputes listed row w with the FP32 activations.
-    static_assert(kRegBlock / 64 == kListLen, "one listed row per wave");
-    __shared__ int final_row[kListLen];
-    __shared__ uint32_t final_key[kListLen];
+    // these lists.  With SPEC (a gate that can ask for verification) the
+    // listed rows' FP32-activation logits go with them.
+    __shared__ float wave_bval[kRegBlock / 64][kListLen];
     const int lane64 = threadIdx.x % 64, wv = threadIdx.x / 64;
     uint64_t best[kListLen];
+    float bval[kListLen];
     uint32_t next = 0;
 #pragma unroll
     for (int r = 0; r <= kListLen; ++r) {
         const uint32_t m = wave_max_u32(tk[0]);
         const int h = __ffsll((unsigned long long)__ballot(tk[0] == m)) - 1;
         const int hrow = __builtin_amdgcn_readlane(trow[0], h);
-        if (r < kListLen)
+        const float hval = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, tval[0]), h));
+        if (r < kListLen) {
             best[r] = (uint64_t)m << 32 | (uint32_t)hrow;
-        else
+            bval[r] = hval;
+        } else {
             next = m;
+        }
         if (lane64 == h) {
 #pragma unroll
             for (int i = 0; i < kListLen; ++i) {
                 tk[i] = tk[i + 1];
                 trow[i] = trow[i + 1];
+                tval[i] = tval[i + 1];
             }
             tk[kListLen] = 0;
         }
     }
     if (lane64 == 0) {
 #pragma unroll
-        for (int r = 0; r < kListLen; ++r)
+        for (int r = 0; r < kListLen; ++r) {
             wave_best[wv][r] = best[r];
+            wave_bval[wv][r] = bval[r];
+        }
         wave_next[wv] = next;
     }
     __syncthreads();
     const int my_slot = list_slot(blockIdx.x);
     if (wv == 0) {
         const uint64_t e = lane64 < (kRegBlock / 64) * kListLen ? wave_best[lane64 / kListLen][lane64 % kListLen] : 0ull;
+        const float ev = lane64 < (kRegBlock / 64) * kListLen ? wave_bval[lane64 / kListLen][lane64 % kListLen] : 0.0f;
         uint32_t ek = (uint32_t)(e >> 32);
         uint32_t nx = wave_max_u32(lane64 < kRegBlock / 64 ? wave_next[lane64] : 0u);
 #pragma unroll
@@ -360,10 +412,11 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
             const int h = __ffsll((unsigned long long)__ballot(ek == m)) - 1;
             if (r < kListLen) {
                 const uint32_t row = __builtin_amdgcn_readlane((uint32_t)e, h);
+                const float val = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ev), h));
                 if (lane64 == 0) {
                     ws->lists[r][my_slot] = (uint64_t)m << 32 | row;
-                    final_row[r] = (int)row;
-                    final_key[r] = m;
+                    if constexpr (SPEC)
+                        ws->list_rec[r][my_slot] = val;
                 }
             } else {
                 nx = max(nx, m);
@@ -373,14 +426,6 @@ __global__ __launch_bounds__(kRegBlock) void k_head_approx(const int8_t* __restr
         }
         if (lane64 == 0)
             ws->lists[kListLen][my_slot] = (uint64_t)nx << 32;
-    }
-    if constexpr (SPEC) {
-        __syncthreads();
-        if (final_key[wv] != 0) {
-            const float r = recompute_row(Q, scale, K, x, final_row[wv]);
-            if (lane64 == 0)
-                ws->list_rec[wv][my_slot] = r;
-        }
     }
 }
 

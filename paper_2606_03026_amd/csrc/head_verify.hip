@@ -74,12 +74,16 @@ int head_verify_forward(const int8_t* Q, const float* scale, int32_t K, int32_t 
     const int64_t wgs = std::max<int64_t>(1, std::min<int64_t>((groups + spk::kRegGroups - 1) / spk::kRegGroups,
                                                                spk::kApproxMaxWgs));
     // a gap is never negative, so only a threshold > 0 can ask for verification:
-    // then the approximate head also recomputes its listed rows
+    // then the approximate head also computes every row's FP32-activation logit
     const bool spec = threshold > 0.0f;
-    hipLaunchKernelGGL(spec ? pick_approx<true>(npl) : pick_approx<false>(npl), dim3((unsigned)wgs),
+    // with the FP32 activations also in registers, K > 2048 leaves room for
+    // one wave per SIMD: the grid is then what fits at once (results do not
+    // depend on the grid)
+    const int64_t grid = spec && npl > 4 ? std::min<int64_t>(wgs, 256) : wgs;
+    hipLaunchKernelGGL(spec ? pick_approx<true>(npl) : pick_approx<false>(npl), dim3((unsigned)grid),
                        dim3(spk::kRegBlock), 0, st, Q, scale, K, V, x, logits, ws);
     hipLaunchKernelGGL(spk::k_head_select, dim3(1), dim3(spk::kSelectBlock), 0, st, logits, V, top_k, threshold,
-                       (int)wgs, (int)spec, ws, Q, scale, K, x, cand, cand_logits, result);
+                       (int)grid, (int)spec, ws, Q, scale, K, x, cand, cand_logits, result);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return hip_fail(e, "head verification launch");

@@ -3,12 +3,13 @@ the CPU oracle.
 
 Exact parts (bit for bit): the approximate logits, the candidate rows and
 their order, the gap and the gate decision, and the approximate candidate
-logits when verification does not run.  FP32 part: the recomputed
-candidate logits, within the bound of the kernel's summation order (a
-per-lane FMA chain of at most 16 ceil(K/1024) products, a 6-level lane
-tree, one multiply): with u = 2^-24, gamma(n) = n u / (1 - n u) and
-h = 16 ceil(K/1024) + 7 (one slack level),
-|rec - exact| <= u |exact| + (1 + u) s_m gamma(h) sum_k |Q x|.
+logits when verification does not run.  FP32 part: the verified candidate
+logits, within the bound of the kernel's summation order (the dense register
+kernel's: a per-lane FMA chain of at most 16 ceil(K/512) products, a 5-level
+lane tree, one multiply): with u = 2^-24, gamma(n) = n u / (1 - n u) and
+h = 16 ceil(K/512) + 6 (one slack level),
+|rec - exact| <= u |exact| + (1 + u) s_m gamma(h) sum_k |Q x|;
+and bit for bit dense_proj_forward's outputs for the candidate rows.
 The token is then the oracle's unless the oracle's best recomputed logits
 lie within twice that bound of each other, where any of the near-tied rows
 is a correct answer.
@@ -51,7 +52,7 @@ def gpu_head(sp, Q, s, x, k, thr, Qd=None):
 
 def rec_bound(Q, s, x, rows):
     K = Q.shape[1]
-    h = 16 * (-(-K // 1024)) + 7
+    h = 16 * (-(-K // 512)) + 6
     gamma = h * U / (1 - h * U)
     absdot = np.abs(Q[rows].astype(np.float64)) @ np.abs(x.astype(np.float64))
     exact = s[rows].astype(np.float64) * (Q[rows].astype(np.float64) @ x.astype(np.float64))
@@ -158,6 +159,48 @@ def test_ties_across_selecting_workgroups(sp, step):
         got = gpu_head(sp, Q, s, x, k, thr)
         ref = assert_head_parity(got, Q, s, x, k, thr)
         assert list(ref["cand"]) == list(range(0, step * k, step))
+
+
+def dense_head_rows(sp, Q, s, x):
+    """dense_proj_forward over all rows of Q for the one activation vector x."""
+    V, K = Q.shape
+    y = torch.full((1, V), float("nan"), dtype=torch.float32, device="cuda")
+    sp.dense_proj_forward(dev(Q), dev(s), dev(x.reshape(1, K)), 1, y)
+    torch.cuda.synchronize()
+    return y[0].cpu().numpy()
+
+
+@pytest.mark.parametrize("V,K", [(57344, 1536), (20000, 1536), (1000, 4096), (3000, 2560), (4097, 96), (65, 1536),
+                                 (3, 48)])
+@pytest.mark.parametrize("k", [2, 16, 64])
+def test_verified_logits_are_the_dense_heads(sp, V, K, k):
+    """The verified candidates' logits are bit for bit the dense register
+    kernel's outputs for those rows (same FMA order), whether they come from
+    the lists or, after a whole-array selection, from the selection's own
+    recompute (ties force that path in the second half)."""
+    k = min(k, V)
+    if (V, K) == (57344, 1536):
+        d = wl.dense_projection("head", B=1)
+        Q, s = d["Q"], d["scale"]
+        x = np.random.default_rng([42, 19, k]).standard_normal(K).astype(np.float32)
+    else:
+        Q, s, x = head_problem(V, K, 7 + k)
+    y = dense_head_rows(sp, Q, s, x)
+    got = gpu_head(sp, Q, s, x, k, float("inf"))
+    assert got["verified"] == (V >= 2)
+    if got["verified"]:
+        np.testing.assert_array_equal(got["cand_logits"].view(np.uint32), y[got["cand"]].view(np.uint32))
+    assert_head_parity(got, Q, s, x, k, float("inf"))
+    if V >= 200:
+        Qt = Q.copy()
+        Qt[::13] = 100  # many equal approximate logits: the lists cannot decide
+        st = np.full(V, 0.003, dtype=np.float32)
+        xt = np.abs(x) + 0.5
+        yt = dense_head_rows(sp, Qt, st, xt)
+        got = gpu_head(sp, Qt, st, xt, k, float("inf"))
+        np.testing.assert_array_equal(got["cand_logits"].view(np.uint32), yt[got["cand"]].view(np.uint32))
+        assert_head_parity(got, Qt, st, xt, k, float("inf"))
+        assert list(got["cand"]) == list(range(0, 13 * k, 13))
 
 
 def test_workspace_shared_by_calls(sp):
