@@ -573,10 +573,23 @@ __device__ inline void radix_select_all(const float* __restrict__ logits, int V,
 }
 
 
+// A pooled entry as one 64-bit code: the logit's key above, the row's
+// complement below, so that a larger code precedes (larger logit, or equal
+// logit and lower row) and one 64-bit compare orders two entries; code 0
+// precedes nothing (key 0 marks "no element").
+__device__ inline uint64_t pool_code(uint32_t key, int row)
+{
+    return (uint64_t)key << 32 | (uint32_t)~row;
+}
+__device__ inline Entry pool_entry(uint64_t code)
+{
+    return Entry{(uint32_t)(code >> 32), (int32_t)~(uint32_t)code};
+}
+
 // Append the lanes' entries with `take` set to the LDS pool: one LDS atomic
 // per wave, positions by lane rank; entries past `cap` are counted, not kept.
 // With `vals`, each entry's value goes to the same position there.
-__device__ inline void pool_append(bool take, uint32_t key, int row, Entry* pool, int* count, int cap,
+__device__ inline void pool_append(bool take, uint32_t key, int row, uint64_t* pool, int* count, int cap,
                                    float val = 0.0f, float* vals = nullptr)
 {
     const uint64_t m = __ballot(take);
@@ -590,7 +603,7 @@ __device__ inline void pool_append(bool take, uint32_t key, int row, Entry* pool
     base = __builtin_amdgcn_readlane(base, first);
     const int pos = base + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
     if (take && pos < cap) {
-        pool[pos] = Entry{key, row};
+        pool[pos] = pool_code(key, row);
         if (vals)
             vals[pos] = val;
     }
@@ -600,11 +613,16 @@ constexpr int kScanUnroll = 16;      // logits per thread loaded before any is u
 constexpr int kMergeCap = 1024;      // pooled entries the selection ranks in LDS
 
 // Rank selection of the kk best of n pooled entries into sel: the rank of
-// an entry is the number of entries that precede it (a strict total order).
-// G threads count for each entry (G the largest power of two up to 64 with
-// G n <= the block), thread p of the group over entries p, p + G, ..., and
-// the G partial counts are summed across the group's lanes.
-__device__ inline void rank_pool(const Entry* pool, int n, int kk, Entry* sel, const float* vals = nullptr,
+// an entry is the number of entries whose code is larger (a strict total
+// order).  The count is bound by vector ALU work (16 waves on the CU's four
+// SIMDs), so each comparison is one 64-bit compare and an add with carry,
+// and the pool past n holds zero codes (kRankPad of them), so that reads
+// need no clamp and counts no mask.  G threads count for each entry (G the
+// largest power of two up to 64 with G n <= the block), thread p of the
+// group over entries p, p + G, ..., and the G partial counts are summed
+// across the group's lanes.
+constexpr int kRankPad = 8;
+__device__ inline void rank_pool(const uint64_t* pool, int n, int kk, Entry* sel, const float* vals = nullptr,
                                  float* sel_vals = nullptr)
 {
     const int tid = threadIdx.x;
@@ -612,26 +630,24 @@ __device__ inline void rank_pool(const Entry* pool, int n, int kk, Entry* sel, c
     while (G < 64 && 2 * G * n <= kSelectBlock)
         G *= 2;
     const int e = tid / G, p = tid % G;
-    Entry me{0u, 0};
+    uint64_t me = 0;
     int rank = 0;
     if (e < n) {
         me = pool[e];
-        // eight LDS reads in flight; past n the last entry is read again and
-        // not counted
-        for (int j = p; j < n; j += 8 * G) {
-            Entry o[8];
+        for (int j = p; j < n; j += 8 * G) {  // eight LDS reads in flight, at most j + 7 G < n + 7 G
+            uint64_t o[8];
 #pragma unroll
             for (int t = 0; t < 8; ++t)
-                o[t] = pool[min(j + t * G, n - 1)];
+                o[t] = pool[j + t * G];
 #pragma unroll
             for (int t = 0; t < 8; ++t)
-                rank += j + t * G < n && precedes(o[t], me);
+                rank += o[t] > me;
         }
     }
     for (int d = 1; d < G; d <<= 1)  // G is the same in every thread
         rank += __shfl_xor(rank, d, 64);
     if (e < n && p == 0 && rank < kk) {
-        sel[rank] = me;
+        sel[rank] = pool_entry(me);
         if (vals)
             sel_vals[rank] = vals[e];
     }
@@ -663,7 +679,9 @@ __global__ __launch_bounds__(kSelectBlock) void k_head_select(const float* __res
                                                               float* __restrict__ cand_logits,
                                                               int32_t* __restrict__ result)
 {
-    __shared__ Entry pool[kMergeCap];
+    // pooled codes, zero past the count: n + 7 G <= kMergeCap + 7 for every
+    // G rank_pool picks
+    __shared__ uint64_t pool[kMergeCap + kRankPad];
     __shared__ float pool_rec[kMergeCap];
     __shared__ Entry sel[kHeadMaxK];
     __shared__ float sel_rec[kHeadMaxK];
@@ -686,6 +704,8 @@ __global__ __launch_bounds__(kSelectBlock) void k_head_select(const float* __res
     for (int i = 0; i < kListLen; ++i)
         erec[i] = spec && b < n_approx ? ws->list_rec[i][tid] : 0.0f;
     uint32_t v = (uint32_t)(ent[0] >> 32);  // the workgroup's largest key
+    for (int i = tid; i < kMergeCap + kRankPad; i += kSelectBlock)
+        pool[i] = 0;
     if (tid == 0)
         s_count = 0;
     uint32_t low = 0xffffffffu;
@@ -736,7 +756,7 @@ __global__ __launch_bounds__(kSelectBlock) void k_head_select(const float* __res
                 const uint32_t k = (uint32_t)(ent[i] >> 32);
                 if (k >= L) {
                     if (pos < kMergeCap) {
-                        pool[pos] = Entry{k, (int32_t)(uint32_t)ent[i]};
+                        pool[pos] = pool_code(k, (int32_t)(uint32_t)ent[i]);
                         pool_rec[pos] = erec[i];
                     }
                     ++pos;
@@ -754,6 +774,8 @@ __global__ __launch_bounds__(kSelectBlock) void k_head_select(const float* __res
     if (!exact) {
         // the lists may miss elements: every logit at or above L
         __syncthreads();
+        for (int i = tid; i < kMergeCap + kRankPad; i += kSelectBlock)
+            pool[i] = 0;
         if (tid == 0)
             s_count = 0;
         __syncthreads();
