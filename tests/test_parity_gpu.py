@@ -640,13 +640,13 @@ def test_every_matrix_core_plan(sp):
 def test_direct_spike_loads_for_the_smallest_batches(sp):
     """Batches of at most 4 rows load their spike words with each k-step
     instead of staging them: every direct plan (K from one word to past 2048,
-    every preload depth and the ring) against the oracle, with junk bits
+    every preload depth and the ring past 6144) against the oracle, with junk bits
     past K, for 1 to 4 rows and channel counts that are and are not a
     multiple of 8 channel sets."""
     direct = {tuple(p.values()) for p in sp.spike_mfma_plans() if p["direct"]}
     assert len(direct) >= 5
     seen = set()
-    for K in (40, 150, 300, 1536, 2111, 6144):
+    for K in (40, 150, 300, 1536, 2111, 6144, 6400):
         for N in (48, 1536):
             for B in (1, 2, 3, 4):
                 path, plan = sp.spike_proj_plan_query(K, N, B)
