@@ -166,7 +166,7 @@ int spike_proj_destroy(spike_proj_t h);
  *   SPIKE_TUNE_MFMA_WAVES   waves per workgroup of the matrix-core path, which
  *                           share one tile's K range: 0 = automatic, 4, 8, 16
  *   SPIKE_TUNE_MFMA_DEPTH   k-steps of weights in flight per wave of the
- *                           matrix-core path: 0 = automatic, 2, 4, 6, 8, 12 (when a
+ *                           matrix-core path: 0 = automatic, 2, 3, 4, 6, 8, 12 (when a
  *                           wave has at most that many k-steps, all of its
  *                           loads are issued at once)
  *   SPIKE_TUNE_MFMA_ROW_TILE  16-row subtiles per matrix-core workgroup:

@@ -509,10 +509,11 @@ constexpr int kMfmaDirectMaxB = 4;
 // Plans also instantiated with direct spike loads: the automatic plans of
 // batches up to kMfmaDirectMaxB rows (one 16-row subtile and one channel set
 // per workgroup; every k-step preloaded up to 6 steps per wave, i.e. for
-// K <= 6144, a ring of 2 beyond).
+// K <= 6144, a ring of 2 beyond; with 8 waves the preload depth equals the
+// wave's step count, so no wave issues a duplicate load).
 #define SPK_MFMA_DIRECT_PLANS(X) \
     X(1, 1, 1, 4, true) X(1, 1, 2, 4, true) X(1, 1, 4, 4, true) X(1, 1, 8, 4, true) X(1, 1, 16, 2, false) \
-    X(1, 1, 16, 6, true)
+    X(1, 1, 16, 6, true) X(1, 1, 8, 1, true) X(1, 1, 8, 2, true) X(1, 1, 8, 3, true)
 
 inline bool mfma_instantiated(const MfmaPlan& p)
 {
@@ -605,6 +606,16 @@ inline MfmaPlan mfma_plan(int K, int N, int B, int rt_req, int cs_req, int kw_re
     if (B <= kMfmaDirectMaxB) {
         MfmaPlan r = p;
         r.direct = true;
+        if (d_req <= 0 && r.preload) {
+            // a depth equal to the step count: a deeper preload re-issues the
+            // last step's loads, which costs a cold call about 0.2 us
+            // (measured on the 44-projection batch-1 chain: 174 us per token
+            // with 3 steps at depth 3 against 179 us at depth 4)
+            MfmaPlan e = r;
+            e.d = (wpr + e.kw - 1) / e.kw;
+            if (mfma_instantiated(e))
+                r = e;
+        }
         if (mfma_instantiated(r))
             p = r;
     }

@@ -696,8 +696,8 @@ int spike_proj_tune(spike_proj_t h, int32_t key, int32_t value)
         h->tiles_per_unit = value;
         return SPIKE_OK;
     case SPIKE_TUNE_MFMA_DEPTH:
-        if (value != 0 && value != 2 && value != 4 && value != 6 && value != 8 && value != 12)
-            return fail(SPIKE_EINVAL, "matrix-core depth must be 0, 2, 4, 6, 8 or 12, got %d", value);
+        if (value != 0 && value != 2 && value != 3 && value != 4 && value != 6 && value != 8 && value != 12)
+            return fail(SPIKE_EINVAL, "matrix-core depth must be 0, 2, 3, 4, 6, 8 or 12, got %d", value);
         h->mfma_depth = value;
         return SPIKE_OK;
     case SPIKE_TUNE_MFMA_WAVES:

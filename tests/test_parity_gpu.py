@@ -646,7 +646,7 @@ def test_direct_spike_loads_for_the_smallest_batches(sp):
     direct = {tuple(p.values()) for p in sp.spike_mfma_plans() if p["direct"]}
     assert len(direct) >= 5
     seen = set()
-    for K in (40, 150, 300, 1536, 2111, 6144, 6400):
+    for K in (40, 150, 300, 512, 1000, 1536, 1900, 2111, 6144, 6400):
         for N in (48, 1536):
             for B in (1, 2, 3, 4):
                 path, plan = sp.spike_proj_plan_query(K, N, B)
