@@ -175,18 +175,26 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
     const __amdgpu_buffer_rsrc_t mrsrc = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint64_t*>(mask), 0, B * wpr * (int)sizeof(uint64_t), kBufferWordFormat);
     // Weights of the wave's step i; DIRECT: also, per row subtile, the dword
-    // holding bits 16q .. 16q + 15 of word s of row 16 ms + c.
+    // holding bits 16q .. 16q + 15 of word s of row 16 ms + c.  A step past
+    // the wave's last (the slots of a preload or ring deeper than the steps
+    // left) is read at the end of the buffer: out of range, so the load
+    // returns zeros and moves no data, where a re-read of the last step
+    // would issue its requests again.  Those slots are never multiplied.
+    const int w_records = (N / 16) * wpr * kMfmaSetStepBytes;
+    const int m_records = B * wpr * (int)sizeof(uint64_t);
     auto load_w = [&](int i, u32x4 (&wv)[CS], uint32_t (&bv)[RT]) {
         const int s = wave + i * KW;
+        const bool live = i < n_steps;
 #pragma unroll
         for (int t = 0; t < CS; ++t)
-            wv[t] = __builtin_amdgcn_raw_buffer_load_b128(prsrc, 16 * l,
-                                                          ((t0 + t) * wpr + s) * kMfmaSetStepBytes, 0);
+            wv[t] = __builtin_amdgcn_raw_buffer_load_b128(
+                prsrc, 16 * l, live ? ((t0 + t) * wpr + s) * kMfmaSetStepBytes : w_records, 0);
         if constexpr (DIRECT) {
 #pragma unroll
             for (int ms = 0; ms < RT; ++ms)
                 bv[ms] = __builtin_amdgcn_raw_buffer_load_b32(
-                    mrsrc, ((m0 + 16 * ms + c) * wpr + s) * (int)sizeof(uint64_t) + 4 * (q / 2), 0, 0);
+                    mrsrc, live ? ((m0 + 16 * ms + c) * wpr + s) * (int)sizeof(uint64_t) + 4 * (q / 2) : m_records, 0,
+                    0);
         }
     };
 
@@ -224,14 +232,14 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
     }
 
     // Every wave has at least one k-step (the plan requires KW <= wpr).
-    // Loads are unconditional, for a step index clamped to the wave's last
-    // step: a conditional load would turn its registers into phis that the
-    // compiler fills with copies.
+    // Loads are unconditional (a step past the wave's last reads out of
+    // range, see load_w): a conditional load would turn its registers into
+    // phis that the compiler fills with copies.
     u32x4 wbuf[D][CS];
     uint32_t bbuf[D][RT];  // DIRECT: the spike dwords of each slot
 #pragma unroll
     for (int d = 0; d < D; ++d)
-        load_w(min(d, n_steps - 1), wbuf[d], bbuf[d]);
+        load_w(d, wbuf[d], bbuf[d]);
 
     // Stage the tile's spike words (ROWS rows x wpr words) unless DIRECT,
     // and zero the partial tile.
@@ -317,13 +325,14 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
             }
     } else if constexpr (DIRECT) {
         // Ring of D slots of weights and spike dwords; a slot is refilled
-        // after its products with the step D ahead (clamped, as below).
+        // after its products with the step D ahead (out of range past the
+        // wave's last step, as below).
         auto step = [&](int i, u32x4 (&wv)[CS], uint32_t (&bv)[RT], bool refill) {
             uint32_t b[RT];
             slot_bits(bv, b);
             products(b, wv);
             if (refill)
-                load_w(min(i + D, n_steps - 1), wv, bv);
+                load_w(i + D, wv, bv);
         };
         const int n_full = n_steps / D * D;
         int i0 = 0;
@@ -339,9 +348,9 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
     } else {
         // Ring of D slots; the loop is unrolled by D so slot indices stay
         // static.  A slot is refilled after its products (the load then
-        // has D - 1 steps of cover) with the step D ahead, clamped to the
-        // wave's last step: an unconditional load keeps the slot out of
-        // phi copies, and the extra loads re-read cached data.  The spike
+        // has D - 1 steps of cover) with the step D ahead, read out of range
+        // past the wave's last step: an unconditional load keeps the slot
+        // out of phi copies, and the extra loads move no data.  The spike
         // bits of the next step are read from LDS one step ahead, so their
         // latency hides behind the current step's products.
         uint32_t bits[RT];
@@ -351,7 +360,7 @@ __device__ __attribute__((always_inline)) inline void mfma_tile(const int8_t* __
             read_bits(min(i + 1, n_steps - 1), nb);
             products(bits, wv);
             if (refill)
-                load_w(min(i + D, n_steps - 1), wv, bv);
+                load_w(i + D, wv, bv);
 #pragma unroll
             for (int ms = 0; ms < RT; ++ms)
                 bits[ms] = nb[ms];
